@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Benchmark of the AR block-sparse attention hot path on one MI355X.
+
+A step is one pass of the whole path over one synthetic batch already resident in HBM:
+la_select_blocks (pool Q, pool+score historical K, select and compact) followed by
+la_sparse_attn_fwd over the kept blocks.  Prints ONE JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+value = kept-block TFLOP/s of the whole step (kept FLOPs / step time).  The line also
+carries the per-kernel split, the dense baseline (same attention kernel, every block
+kept), the roofline of the attention kernel and the fp64 oracle's CPU rate.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+HBM_PEAK_GBS = 8000.0              # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="480p_window")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup + steps of the sparse path only (for rocprofv3), print the JSON anyway")
+    return ap.parse_args()
+
+
+def src_digest(*names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2605_31158_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel_tag: str, workload: str, digest: str, launches_bytes: float):
+    """HBM bytes per launch measured by rocprofv3 PMC runs of the current kernel source, or None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_tag}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("src_digest") != digest:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, inp, mask_np, target_s: float):
+    """The fp64 oracle on the host: selection of one head plus attention of as many of its
+    query blocks as fit in about target_s seconds; rate in kept TFLOP/s."""
+    from oracle import la_oracle as O
+    threads = None
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max((i.get("num_threads", 1) for i in info), default=1)
+    except Exception:
+        pass
+    t0 = time.perf_counter()
+    sel = O.select_blocks(inp["q"][:, :1], inp["k"][:, :1], wl.block, tau=wl.tau)
+    t_sel = time.perf_counter() - t0
+    flops = 0
+    rows_done = 0
+    t1 = time.perf_counter()
+    i = 0
+    while i < wl.nq:
+        chunk = list(range(i, min(i + 8, wl.nq)))
+        O.attention_rows(inp["q"], inp["k"], inp["v"], mask_np, wl.block, [(0, 0, r) for r in chunk],
+                         frame_tokens=wl.frame_tokens if wl.causal_frames else 0)
+        for r in chunk:
+            lo, hi = r * wl.block, min((r + 1) * wl.block, wl.Lq)
+            nk = sum(min((m + 1) * wl.block, wl.Lk) - m * wl.block for m in np.nonzero(mask_np[0, 0, r])[0])
+            flops += 4 * wl.d * (hi - lo) * nk
+        rows_done += len(chunk)
+        i += len(chunk)
+        if time.perf_counter() - t1 > target_s:
+            break
+    t_attn = time.perf_counter() - t1
+    # selection share of one query block of this head, added pro rata
+    t_total = t_attn + t_sel * rows_done / wl.nq
+    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": threads or os.cpu_count(),
+            "kind": "oracle",
+            "sample": f"head 0 of {wl.name}: selection over its {wl.nq} query blocks (pro rata) + fp64 attention of "
+                      f"{rows_done}/{wl.nq} query blocks on the GPU's mask; {flops / 1e9:.1f} GFLOP kept in "
+                      f"{t_total:.1f} s; os.cpu_count()={os.cpu_count()}, "
+                      f"affinity={len(os.sched_getaffinity(0))}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (one GPU's share of the "
+              "heads is the unit of work). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2605_31158_amd import la
+    from paper_2605_31158_amd.workloads import WORKLOADS, make_inputs
+
+    wl = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    inp = make_inputs(wl)
+    g = {x: la.bf16_from_bits(inp[x], dev) for x in "qkv"}
+    t_gen = time.perf_counter() - t_gen
+    B, H, Lq, d = wl.B, wl.H, wl.Lq, wl.d
+    NQ, NK = wl.nq, wl.nk
+    F = wl.frame_tokens if wl.causal_frames else 0
+    shape = la.make_shape(B, H, Lq, wl.Lk, d, wl.block, wl.n_text, F)
+    ws = torch.empty(max(la.workspace_bytes(shape), 256), dtype=torch.uint8, device=dev)
+    mask = torch.empty((B, H, NQ, NK), dtype=torch.uint8, device=dev)
+    counts = torch.empty((B, H, NQ), dtype=torch.int32, device=dev)
+    idx = torch.empty((B, H, NQ, NK), dtype=torch.int32, device=dev)
+    o = torch.empty_like(g["q"])
+    stream = torch.cuda.current_stream(dev)
+
+    def select():
+        la.select_blocks(g["q"], g["k"], wl.block, wl.tau, n_text=wl.n_text, ws=ws, out=(mask, counts, idx))
+
+    def attn(cnt, ix):
+        la.sparse_attn_fwd(g["q"], g["k"], g["v"], cnt, ix, wl.block, n_text=wl.n_text, frame_tokens=F,
+                           ws=ws, out=o)
+
+    for _ in range(args.warmup):
+        select()
+        attn(counts, idx)
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for it in range(K):
+        ev[it][0].record(stream)
+        select()
+        ev[it][1].record(stream)
+        attn(counts, idx)
+        ev[it][2].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / K
+    t_sel = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(K)])
+    t_att = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(K)])
+
+    mask_np = mask.cpu().numpy()
+    nq_valid = np.array([min((i + 1) * wl.block, Lq) - i * wl.block for i in range(NQ)], np.int64)
+    nk_valid = np.array([min((m + 1) * wl.block, wl.Lk) - m * wl.block for m in range(NK)], np.int64)
+    kept_flops = float(4 * d * np.einsum("xij,i,j->", mask_np.reshape(-1, NQ, NK).astype(np.int64),
+                                         nq_valid, nk_valid))
+    dense_flops = 4.0 * B * H * Lq * wl.Lk * d
+    rho = kept_flops / dense_flops
+
+    # dense baseline: the same attention kernel over every key block
+    dense_ms = None
+    if not args.no_dense and not args.profile_only:
+        dmask = torch.ones_like(mask)
+        dcounts, didx = la.mask_to_list(dmask, wl.block, Lq, wl.Lk, d)
+        for _ in range(3):
+            attn(dcounts, didx)
+        torch.cuda.synchronize()
+        nd = max(3, min(K, 20))
+        evd = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nd)]
+        for it in range(nd):
+            evd[it][0].record(stream)
+            attn(dcounts, didx)
+            evd[it][1].record(stream)
+        torch.cuda.synchronize()
+        dense_ms = float(np.median([evd[i][0].elapsed_time(evd[i][1]) for i in range(nd)]))
+        del dmask, dcounts, didx
+
+    sel_ms = float(np.mean(t_sel))
+    att_ms = float(np.mean(t_att))
+    value = kept_flops / (ms_step * 1e-3) / 1e12
+    achieved = kept_flops / (att_ms * 1e-3) / 1e12
+    hbm_sel_bytes = 2.0 * B * H * (Lq + (wl.Lk - Lq - wl.n_text)) * d + mask_np.size * (1 + 4) + counts.numel() * 4
+    digest = src_digest("attn.hip")
+    traffic = traffic_from_profile("attn_fwd", wl.name, digest, kept_flops)
+
+    out = {
+        "metric": "sparse AR attention kept-block TFLOP/s (select + sparse attention per call)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "H": H, "d": d, "Lq": Lq, "Lk": wl.Lk, "block": wl.block,
+                   "tau": wl.tau, "frame_causal": bool(F), "seed": wl.seed},
+        "select_ms": round(sel_ms, 4),
+        "attn_ms": round(att_ms, 4),
+        "attn_ms_p10_p90": [round(float(np.percentile(t_att, 10)), 4), round(float(np.percentile(t_att, 90)), 4)],
+        "keep_ratio": round(rho, 5),
+        "kept_tflop": round(kept_flops / 1e12, 5),
+        "attn_tflops": round(achieved, 2),
+        "attn_pct_mfma_peak": round(100 * achieved / MFMA_BF16_PEAK_TFLOPS, 2),
+        "select_gbs": round(hbm_sel_bytes / (sel_ms * 1e-3) / 1e9, 1),
+        "dense_attn_ms": None if dense_ms is None else round(dense_ms, 4),
+        "dense_tflops": None if dense_ms is None else round(dense_flops / (dense_ms * 1e-3) / 1e12, 2),
+        "speedup_vs_dense": None if dense_ms is None else round(dense_ms / (sel_ms + att_ms), 3),
+        "ideal_speedup": round(1.0 / rho, 3),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": traffic, "kernel": "attn_fwd_kernel<128>", "src_digest": digest},
+        "gpu": torch.cuda.get_device_name(dev),
+        "gen_s": round(t_gen, 2),
+    }
+    if not args.no_cpu_baseline and not args.profile_only:
+        out["cpu_baseline"] = cpu_baseline(wl, inp, mask_np, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,136 @@
+/*
+ * la.h -- C ABI of libla: block selection and block-sparse attention for
+ * autoregressive (AR) chunk generation on AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the "hardware-software co-designed 3D block sparse attention"
+ * of Light Interaction (Sec. 3.3): a chunk of Lq query tokens (the frames being
+ * denoised) attends to Lk keys laid out as
+ *     [n_text text tokens][historical visual context][current chunk: last Lq keys].
+ * Tokens are cut into 1-D blocks of `block` consecutive tokens.  Per (batch, head,
+ * query block i) the library
+ *   1. pools each query block and each historical key block into its mean
+ *      (Sec. 3.3, pooling equation);
+ *   2. scores s_{i,m} = q_bar_i . k_bar_m / sqrt(d) over the M historical blocks
+ *      (Sec. 3.3, selection equation);
+ *   3. keeps a subset S_i of the historical blocks: either the shortest
+ *      highest-scoring prefix whose softmax mass over the M scores reaches tau
+ *      (la_select_blocks), or the floor(r*M) highest scores, the paper's own
+ *      Top-floor(rM) rule (la_select_blocks_topk);
+ *   4. attends over C_i = text blocks u current-chunk blocks u S_i (Sec. 3.3,
+ *      context-union equation), the same block set for K and V.
+ *
+ * Conventions shared by every call
+ *   - Tensors are device pointers, contiguous, row-major, layout [B, H, L, d]
+ *     for q, k, v and o; bf16 is raw IEEE bfloat16 (16-bit), 16-byte aligned.
+ *   - The caller owns every buffer.  The library allocates no memory and keeps
+ *     no state between calls; scratch space comes in through `ws`/`ws_bytes`
+ *     (size from la_workspace_bytes; 256-byte alignment).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream) and the
+ *     call returns without synchronising.  Outputs are ready when the stream is.
+ *   - Arguments are validated before anything is enqueued: on any error the call
+ *     returns a non-zero la_status and enqueues nothing, writes nothing.
+ *     LA_ERR_HIP reports a failed kernel launch (outputs are then undefined).
+ *   - No floating-point atomics: results are bit-reproducible run to run.
+ *   - Calls are thread-safe (no global state).
+ */
+#ifndef LA_H_
+#define LA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum la_status {
+  LA_OK = 0,
+  LA_ERR_ARG = 1,        /* null pointer, tau <= 0 or NaN, bad r, misaligned pointer */
+  LA_ERR_SHAPE = 2,      /* unsupported or inconsistent shape (see la_shape) */
+  LA_ERR_WORKSPACE = 3,  /* ws too small or NULL while needed */
+  LA_ERR_HIP = 4         /* a HIP launch failed */
+} la_status;
+
+/* Problem shape.
+ *   B, H        batch and heads (>= 1); every (b, h) is independent (Sec. 3.3:
+ *               pooling and selection run per attention head).
+ *   Lq, Lk      query tokens and key tokens, 1 <= Lq <= Lk - n_text.
+ *   d           head dimension: 64 or 128.
+ *   block       tokens per block, the same tiling for queries and keys: 64 or 128.
+ *               NQ = ceil(Lq/block) query blocks, NK = ceil(Lk/block) key blocks.
+ *   n_text      leading text-condition keys, always kept (the paper's T).
+ *   frame_tokens  0: every kept key is visible to every query.  F > 0: frame-causal
+ *               inside the chunk, query token t (chunk position) sees chunk key
+ *               n (n >= Lk - Lq) only if (n - (Lk - Lq)) / F <= t / F; context keys
+ *               stay visible.  Used by la_sparse_attn_fwd only.
+ * Key block m is forced (always kept, never scored) when it overlaps the text
+ * tokens [0, n_text) or the chunk [Lk - Lq, Lk); the others are the M historical
+ * candidates, block indices [ceil(n_text/block), floor((Lk-Lq)/block)).
+ * Limits: NK <= 16384, M <= 4096, B*H <= 65535. */
+typedef struct la_shape {
+  int32_t B, H, Lq, Lk, d;
+  int32_t block;
+  int32_t n_text;
+  int32_t frame_tokens;
+} la_shape;
+
+/* Bytes of scratch space la_select_blocks, la_select_blocks_topk and
+ * la_sparse_attn_fwd need for this shape (the maximum over the three).
+ * Returns 0 for an invalid shape. */
+size_t la_workspace_bytes(const la_shape* shape);
+
+/* Cumulative-mass block selection.
+ *   q      bf16 [B, H, Lq, d];  k  bf16 [B, H, Lk, d]      (inputs)
+ *   tau    in (0, +inf): per query block keep the shortest prefix of historical
+ *          blocks, ordered by score descending (lower block index first on equal
+ *          scores), whose softmax mass (softmax over the M scores) is >= tau.
+ *          tau >= 1 keeps every historical block.
+ *   mask   uint8 [B, H, NQ, NK] or NULL: 1 = key block kept, 0 = skipped.
+ *   counts int32 [B, H, NQ]: number of kept key blocks per query block.
+ *   idx    int32 [B, H, NQ, NK]: per query block, the kept key-block indices in
+ *          ascending order in the first counts[] slots; later slots untouched.
+ * Returns LA_ERR_ARG for tau <= 0 or NaN. */
+la_status la_select_blocks(const la_shape* shape, const void* q, const void* k, float tau,
+                           uint8_t* mask, int32_t* counts, int32_t* idx,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* The paper's Top-floor(rM) rule (Sec. 3.3, selection equation): keep the
+ * keep_blocks = floor(r*M) highest-scoring historical blocks, computed by the
+ * caller and clamped to [0, M] here (0 keeps only the forced blocks).  Same
+ * outputs as la_select_blocks.  keep_blocks < 0 is LA_ERR_ARG. */
+la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void* k,
+                                int32_t keep_blocks, uint8_t* mask, int32_t* counts,
+                                int32_t* idx, void* ws, size_t ws_bytes, void* stream);
+
+/* Block-sparse attention forward over the kept blocks.
+ *   q bf16 [B, H, Lq, d]; k, v bf16 [B, H, Lk, d]                 (inputs)
+ *   counts int32 [B, H, NQ], idx int32 [B, H, NQ, NK]: kept key blocks per query
+ *          block, strictly ascending, each in [0, NK) (as written by
+ *          la_select_blocks or la_mask_to_list; other lists are undefined
+ *          behaviour).  One list serves both K and V (Sec. 3.3).
+ *   scale  logit scale; <= 0 selects 1/sqrt(d).
+ *   o      bf16 [B, H, Lq, d]: o_t = sum_n softmax_n(q_t . k_n * scale) v_n over
+ *          the keys of the kept blocks visible to t; 0 when none is.
+ *   lse    float [B, H, Lq] or NULL: natural-log sum of exp(logits) per query
+ *          token, -inf when no key is visible.
+ * Softmax in fp32, products in bf16 with fp32 accumulation. */
+la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k, const void* v,
+                             const int32_t* counts, const int32_t* idx, float scale,
+                             void* o, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Compacts a block mask (uint8 [B, H, NQ, NK], non-zero = kept) into the
+ * counts/idx form la_sparse_attn_fwd reads.  Needs no workspace. */
+la_status la_mask_to_list(const la_shape* shape, const uint8_t* mask, int32_t* counts,
+                          int32_t* idx, void* stream);
+
+/* Static description of a status code. */
+const char* la_status_string(la_status status);
+
+/* ABI version of this header: 1. */
+int32_t la_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LA_H_ */

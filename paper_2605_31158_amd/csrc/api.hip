@@ -1,0 +1,129 @@
+// Host side of the C ABI declared in include/la.h: argument validation, workspace
+// sizing and kernel launches.  Nothing here allocates device memory.
+#include <math.h>
+
+#include "la_internal.h"
+
+namespace la {
+
+la_status make_dims(const la_shape* s, Dims* o) {
+  if (!s) return LA_ERR_ARG;
+  if (s->B < 1 || s->H < 1 || s->Lq < 1 || s->Lk < 1) return LA_ERR_SHAPE;
+  if (s->d != 64 && s->d != 128) return LA_ERR_SHAPE;
+  if (s->block != 64 && s->block != 128) return LA_ERR_SHAPE;
+  if (s->n_text < 0 || s->frame_tokens < 0) return LA_ERR_SHAPE;
+  if ((int64_t)s->Lq + s->n_text > (int64_t)s->Lk) return LA_ERR_SHAPE;
+  // int32 element offsets inside one (b, h) slice and grid limits
+  if ((int64_t)s->Lk * s->d >= (int64_t(1) << 31)) return LA_ERR_SHAPE;
+  if ((int64_t)s->B * s->H >= 65536) return LA_ERR_SHAPE;
+  o->B = s->B; o->H = s->H; o->Lq = s->Lq; o->Lk = s->Lk; o->d = s->d; o->block = s->block;
+  o->n_text = s->n_text; o->frame_tokens = s->frame_tokens;
+  o->BH = s->B * s->H;
+  o->NQ = ceil_div(s->Lq, s->block);
+  o->NK = ceil_div(s->Lk, s->block);
+  if (o->NK > kMaxKeyBlocks) return LA_ERR_SHAPE;
+  o->chunk0 = s->Lk - s->Lq;
+  o->h0 = ceil_div(s->n_text, s->block);
+  o->h1 = o->chunk0 / s->block;
+  if (o->h1 < o->h0) o->h1 = o->h0;
+  o->M = o->h1 - o->h0;
+  if (o->M > kMaxCandidates) return LA_ERR_SHAPE;
+  return LA_OK;
+}
+
+size_t select_ws_bytes(const Dims& dm) {
+  size_t qbar = (size_t)dm.BH * dm.NQ * dm.d * sizeof(float);
+  size_t scores = (size_t)dm.BH * dm.NQ * (size_t)(dm.M > 0 ? dm.M : 1) * sizeof(float);
+  return align256(qbar) + align256(scores);
+}
+
+size_t attn_ws_bytes(const Dims& dm, int splits) {
+  if (splits <= 1) return 0;
+  size_t rows = (size_t)splits * dm.BH * dm.Lq;
+  return align256(rows * dm.d * sizeof(float)) + 2 * align256(rows * sizeof(float));
+}
+
+}  // namespace la
+
+using namespace la;
+
+static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
+extern "C" {
+
+size_t la_workspace_bytes(const la_shape* shape) {
+  Dims dm;
+  if (make_dims(shape, &dm) != LA_OK) return 0;
+  size_t a = select_ws_bytes(dm);
+  size_t b = attn_ws_bytes(dm, attn_splits(dm));
+  return a > b ? a : b;
+}
+
+static la_status select_common(const la_shape* shape, const void* q, const void* k, float tau,
+                               int keep_fixed, uint8_t* mask, int32_t* counts, int32_t* idx,
+                               void* ws, size_t ws_bytes, void* stream) {
+  Dims dm;
+  la_status st = make_dims(shape, &dm);
+  if (st != LA_OK) return st;
+  if (!q || !k || !counts || !idx) return LA_ERR_ARG;
+  if (misaligned(q) || misaligned(k)) return LA_ERR_ARG;
+  if (!ws || ws_bytes < select_ws_bytes(dm) || ((uintptr_t)ws & 255u)) return LA_ERR_WORKSPACE;
+  hipError_t e = launch_select(dm, q, k, tau, keep_fixed, mask, counts, idx, ws, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_select_blocks(const la_shape* shape, const void* q, const void* k, float tau,
+                           uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (!(tau > 0.0f)) return LA_ERR_ARG;   // also rejects NaN
+  return select_common(shape, q, k, tau, -1, mask, counts, idx, ws, ws_bytes, stream);
+}
+
+la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void* k, int32_t keep_blocks,
+                                uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, size_t ws_bytes,
+                                void* stream) {
+  if (keep_blocks < 0) return LA_ERR_ARG;
+  return select_common(shape, q, k, 1.0f, keep_blocks, mask, counts, idx, ws, ws_bytes, stream);
+}
+
+la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k, const void* v,
+                             const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
+                             void* ws, size_t ws_bytes, void* stream) {
+  Dims dm;
+  la_status st = make_dims(shape, &dm);
+  if (st != LA_OK) return st;
+  if (!q || !k || !v || !counts || !idx || !o) return LA_ERR_ARG;
+  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return LA_ERR_ARG;
+  if (isnan(scale) || isinf(scale)) return LA_ERR_ARG;
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)dm.d);
+  int splits = attn_splits(dm);
+  size_t need = attn_ws_bytes(dm, splits);
+  if (need > 0 && (!ws || ws_bytes < need || ((uintptr_t)ws & 255u))) return LA_ERR_WORKSPACE;
+  hipError_t e = launch_attn(dm, q, k, v, counts, idx, scale, o, lse, ws, splits, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_mask_to_list(const la_shape* shape, const uint8_t* mask, int32_t* counts, int32_t* idx,
+                          void* stream) {
+  Dims dm;
+  la_status st = make_dims(shape, &dm);
+  if (st != LA_OK) return st;
+  if (!mask || !counts || !idx) return LA_ERR_ARG;
+  hipError_t e = launch_mask_to_list(dm, mask, counts, idx, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+const char* la_status_string(la_status s) {
+  switch (s) {
+    case LA_OK: return "ok";
+    case LA_ERR_ARG: return "invalid argument";
+    case LA_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case LA_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case LA_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+int32_t la_abi_version(void) { return 1; }
+
+}  // extern "C"

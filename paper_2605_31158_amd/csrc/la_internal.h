@@ -1,0 +1,51 @@
+// Internal declarations shared by the HIP translation units of libla (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "la.h"
+
+namespace la {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+
+constexpr int kMaxCandidates = 4096;   // M limit of the selection sort (LDS-resident)
+constexpr int kMaxKeyBlocks = 16384;   // NK limit (per-row flags live in LDS)
+
+// Shape-derived quantities every entry point needs.
+struct Dims {
+  int B, H, Lq, Lk, d, block, n_text, frame_tokens;
+  int BH, NQ, NK;
+  int h0, h1, M;      // historical candidates are key blocks [h0, h1), M = h1 - h0
+  int chunk0;         // first chunk key: Lk - Lq
+};
+
+__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Validates the shape and fills Dims; LA_OK or LA_ERR_SHAPE.
+la_status make_dims(const la_shape* s, Dims* out);
+
+// Workspace layout of the selection pass: pooled queries then the score matrix.
+size_t select_ws_bytes(const Dims& dm);
+// Workspace of the attention pass for a given split count (partials + row stats).
+size_t attn_ws_bytes(const Dims& dm, int splits);
+// Split factor the attention pass uses for this shape (1 = no split).
+int attn_splits(const Dims& dm);
+
+// Launchers (defined next to their kernels); they only enqueue.
+hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau, int keep_fixed,
+                         uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st);
+hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,
+                               hipStream_t st);
+hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void* v,
+                       const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
+                       void* ws, int splits, hipStream_t st);
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace la

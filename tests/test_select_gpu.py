@@ -1,0 +1,111 @@
+"""GPU block selection vs the fp64 oracle: bit-exact mask outside the ambiguity band,
+counts and lists consistent with the mask, and a valid selection everywhere."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import la_oracle as O
+from paper_2605_31158_amd import la
+from paper_2605_31158_amd.workloads import WORKLOADS, CONFIG_ORDER, make_inputs, make_clustered
+from helpers import say, to_gpu, check_list, check_selection
+
+pytestmark = pytest.mark.gpu
+
+
+def run_select(inp, block, tau=None, keep=None, n_text=0):
+    g = to_gpu(inp)
+    if keep is None:
+        mask, counts, idx = la.select_blocks(g["q"], g["k"], block, tau, n_text=n_text)
+    else:
+        mask, counts, idx = la.select_blocks_topk(g["q"], g["k"], block, keep, n_text=n_text)
+    torch.cuda.synchronize()
+    return mask.cpu().numpy(), counts.cpu().numpy(), idx.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", CONFIG_ORDER + ["480p_long_dense"])
+def test_select_named_workloads(name):
+    wl = WORKLOADS[name]
+    say(f"[select] {name} shape B={wl.B} H={wl.H} Lq={wl.Lq} Lk={wl.Lk} d={wl.d} block={wl.block} tau={wl.tau}")
+    inp = make_inputs(wl)
+    mask, counts, idx = run_select(inp, wl.block, tau=wl.tau)
+    sel = O.select_blocks(inp["q"], inp["k"], wl.block, tau=wl.tau)
+    check_selection(mask, sel)
+    check_list(mask, counts, idx)
+    say(f"[select] {name} ok: kept blocks {int(mask.sum())}, oracle {int(sel['mask'].sum())}, "
+        f"differ {int((mask != sel['mask']).sum())} (all inside the band)")
+
+
+EDGE = [
+    # (B, H, Lq, Lk, d, block, n_text, tau, seed, kind)
+    (1, 2, 64, 640, 64, 64, 0, 0.9, 1, "Lq = one block"),
+    (2, 3, 100, 900, 128, 64, 0, 0.7, 2, "ragged q and k blocks"),
+    (1, 2, 200, 1100, 64, 128, 0, 0.9, 3, "block 128 ragged"),
+    (1, 2, 256, 256, 64, 64, 0, 0.9, 4, "M = 0"),
+    (1, 2, 200, 330, 128, 64, 0, 0.5, 5, "chunk start inside a block"),
+    (1, 2, 128, 4096, 64, 64, 70, 0.9, 6, "text tokens"),
+    (1, 2, 128, 4096, 64, 64, 0, 1e-6, 7, "tau -> 0+"),
+    (1, 2, 128, 4096, 64, 64, 0, 1.0, 8, "tau = 1"),
+    (1, 2, 128, 4096, 64, 64, 0, 3.0, 9, "tau > 1"),
+    (1, 1, 64, 64 * 4097, 64, 64, 0, 0.95, 10, "M = 4096 (largest)"),
+    (1, 4, 300, 64 * 700, 128, 64, 0, 0.99, 11, "M = 695, peaky"),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[c[-1] for c in EDGE])
+def test_select_edge_shapes(case):
+    B, H, Lq, Lk, d, block, n_text, tau, seed, kind = case
+    say(f"[select-edge] {kind}: B={B} H={H} Lq={Lq} Lk={Lk} d={d} block={block} n_text={n_text} tau={tau}")
+    inp = make_clustered(B, H, Lq, Lk, d, block, seed, n_text=n_text)
+    mask, counts, idx = run_select(inp, block, tau=tau, n_text=n_text)
+    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau, n_text=n_text)
+    check_selection(mask, sel)
+    check_list(mask, counts, idx)
+
+
+def test_select_tied_scores():
+    # duplicated key blocks give exactly tied scores: lower block index wins inside the band
+    B, H, Lq, Lk, d, block = 1, 2, 128, 2048, 64, 64
+    inp = make_clustered(B, H, Lq, Lk, d, block, 12)
+    k = inp["k"].copy()
+    k[:, :, 64 * 5:64 * 6] = k[:, :, 64 * 3:64 * 4]      # block 5 = block 3
+    k[:, :, 64 * 9:64 * 10] = k[:, :, 64 * 3:64 * 4]     # block 9 = block 3
+    inp["k"] = k
+    for tau in (0.3, 0.9):
+        mask, counts, idx = run_select(inp, block, tau=tau)
+        sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau)
+        check_selection(mask, sel)
+        check_list(mask, counts, idx)
+
+
+@pytest.mark.parametrize("r", [0.0, 0.175, 0.5, 1.0])
+def test_select_topk(r):
+    # the paper's Top-floor(rM) rule, keep = floor(r * M) computed on the host
+    B, H, Lq, Lk, d, block = 1, 4, 384, 64 * 160, 128, 64
+    inp = make_clustered(B, H, Lq, Lk, d, block, 13)
+    M = (Lk - Lq) // block
+    keep = int(np.floor(r * M + 1e-9))
+    say(f"[select-topk] r={r} M={M} keep={keep}")
+    mask, counts, idx = run_select(inp, block, keep=keep)
+    sel = O.select_blocks(inp["q"], inp["k"], block, topk_r=r)
+    check_selection(mask, sel)
+    check_list(mask, counts, idx)
+
+
+def test_select_deterministic():
+    wl = WORKLOADS["tiny"]
+    inp = make_inputs(wl)
+    a = run_select(inp, wl.block, tau=wl.tau)
+    b = run_select(inp, wl.block, tau=wl.tau)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_mask_to_list_random():
+    rng = np.random.default_rng(14)
+    B, H, NQ, NK = 2, 3, 5, 37
+    mask = (rng.uniform(size=(B, H, NQ, NK)) < 0.3).astype(np.uint8)
+    mask[0, 0, 0] = 0
+    mask[1, 2, 4] = 1
+    counts, idx = la.mask_to_list(torch.from_numpy(mask).cuda(), 64, Lq=NQ * 64 - 10, Lk=NK * 64 - 5)
+    torch.cuda.synchronize()
+    check_list(mask, counts.cpu().numpy(), idx.cpu().numpy())
