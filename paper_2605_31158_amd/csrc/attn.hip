@@ -8,8 +8,9 @@
 //     order (a two-pointer merge over the sorted lists).  Every kept block is staged once in
 //     LDS and consumed by the waves whose query block kept it; the other waves only help
 //     load.  Forced (chunk) blocks are kept by every query block, so most tiles are shared.
-//   * Key blocks are consumed in 64-key sub-tiles.  Sub-tile t+1 is fetched from global
-//     memory into registers while sub-tile t is multiplied (register double buffering).
+//   * Key blocks are consumed in 64-key sub-tiles, staged by asynchronous direct-to-LDS
+//     16-byte loads into a double buffer: sub-tile t+1 streams in while sub-tile t is
+//     multiplied, with one workgroup barrier per sub-tile.
 //   * Workgroup ids are remapped so that each XCD (each L2) works on consecutive (head,
 //     row tile) units: the kept K/V blocks of a head stay hot in one XCD's L2.
 //   * Few work units (small problems) split the key-block range across workgroups; the
@@ -17,12 +18,13 @@
 //
 // Per wave and 64-key sub-tile (d = 128):
 //   S^T (64 keys x 32 queries) = K_tile (64 x d) . Q^T       32 x v_mfma_f32_16x16x32_bf16
-//   online softmax over keys (fp32, base-2 exponent, running max m and sum l per query)
+//   online softmax over keys (fp32, base 2; the running max is only raised when a tile's
+//   max exceeds it by more than 2^8, so most tiles skip the rescale of O)
 //   O^T (d x 32) += V^T (d x 64) . P^T (64 x 32)              32 x v_mfma_f32_16x16x32_bf16
 // S^T is computed transposed so that its accumulator layout (each lane holds 4 consecutive
-// keys of one query column) is directly the B operand of the P.V product.  V is written
-// transposed into LDS, with the 64 keys of a sub-tile permuted so that the 8 keys a lane
-// needs for one MFMA k-step are contiguous (one 16-byte LDS read per operand).
+// keys of one query column) is directly the B operand of the P.V product.  K and V tiles are
+// row-major in LDS with a per-row XOR swizzle of the 16-byte chunks (conflict-free operand
+// reads); the V^T operand is read with the LDS transpose load ds_read_b64_tr_b16.
 #include <math.h>
 
 #include "la_internal.h"
@@ -35,18 +37,13 @@ constexpr int KT = 64;          // keys per sub-tile
 constexpr int QW = 32;          // query rows per wave
 constexpr int QR = 128;         // query rows per workgroup
 constexpr int kEnd = 0x7fffffff;
+constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the running max is raised
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+#define LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 __device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-// Position of key kk (0..63) of a sub-tile inside the transposed V row: the 8 keys
-// {32ks + 16h + 4g + i : h in {0,1}, i in 0..3} a lane multiplies in k-step ks land at
-// positions 32ks + 8g + 4h + i.
-__device__ inline int vpos(int kk) {
-  const int ks = kk >> 5, rem = kk & 31;
-  const int h = rem >> 4, g = (rem & 15) >> 2, i = rem & 3;
-  return (ks << 5) + (g << 3) + (h << 2) + i;
 }
 
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
@@ -54,62 +51,43 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
+// Per-row XOR swizzle of the 16-byte chunks of a tile row.  Chosen so that (a) the 16 rows
+// one MFMA operand read touches map a fixed chunk to 16 distinct bank groups and (b) the
+// transpose reads of V (8 rows x 2 adjacent chunks per half-wave) are conflict-free.
 template <int D>
-struct Smem {
-  static constexpr int KLD = D + 8;     // bf16 elements per K row in LDS (16-byte pad)
-  static constexpr int VLD = KT + 8;    // bf16 elements per transposed-V row in LDS
-  uint16_t k[KT * KLD];
-  uint16_t vt[D * VLD];
-};
-
-template <int D>
-struct TileRegs {
-  static constexpr int CH = D / 8;                 // 16-byte chunks per row
-  static constexpr int N = KT * CH / kThreads;     // 16-byte loads per thread per matrix
-  u32x4 k[N];
-  u32x4 v[N];
-};
-
-// Global -> registers for one 64-key sub-tile starting at key `key0` (rows >= Lk read as 0).
-template <int D>
-__device__ inline void fetch_tile(TileRegs<D>& r, const uint16_t* __restrict__ kh,
-                                  const uint16_t* __restrict__ vh, int key0, int Lk) {
-  constexpr int CH = TileRegs<D>::CH;
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int n = 0; n < TileRegs<D>::N; ++n) {
-    // K: 16 B chunks row-major, consecutive threads along a row
-    const int u = tid + n * kThreads;
-    const int kk = u / CH, ch = u % CH;
-    const int key = key0 + kk;
-    r.k[n] = key < Lk ? *(const u32x4*)(kh + (size_t)key * D + ch * 8) : u32x4{0u, 0u, 0u, 0u};
-    // V: 16 consecutive keys x 4 chunks per wave (64-byte row segments)
-    const int kv = (u & 15) + 16 * (u / (16 * CH));
-    const int cv = (u >> 4) % CH;
-    const int keyv = key0 + kv;
-    r.v[n] = keyv < Lk ? *(const u32x4*)(vh + (size_t)keyv * D + cv * 8) : u32x4{0u, 0u, 0u, 0u};
-  }
+__device__ inline int swz(int r) {
+  if constexpr (D == 128) return ((r & 7) << 1) | ((r >> 3) & 1);
+  else return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
 }
 
-// Registers -> LDS: K row-major (padded rows), V transposed with the vpos() permutation.
 template <int D>
-__device__ inline void store_tile(Smem<D>& sm, const TileRegs<D>& r) {
-  constexpr int CH = TileRegs<D>::CH;
-  constexpr int KLD = Smem<D>::KLD, VLD = Smem<D>::VLD;
-  const int tid = threadIdx.x;
+struct Tile {
+  static constexpr int CH = D / 8;                 // 16-byte chunks per row
+  static constexpr int ROWB = D * 2;               // bytes per row
+  static constexpr int RPI = 64 / CH;              // rows one wave-wide 1 KiB load covers
+  static constexpr int NI = KT / (RPI * 4);        // loads per thread per matrix per sub-tile
+  static constexpr int BYTES = KT * ROWB;          // one matrix sub-tile
+};
+
+// Issues the direct-to-LDS loads of one K and one V sub-tile (64 keys from key0; rows past
+// Lk re-read row Lk-1, their logits are masked).  Lane l of a wave-wide load lands at
+// dst + 16 l, so the swizzle is applied by choosing which global chunk each lane fetches.
+template <int D>
+__device__ inline void issue_tile(unsigned char* kdst, unsigned char* vdst, const uint16_t* __restrict__ kh,
+                                  const uint16_t* __restrict__ vh, int key0, int Lk) {
+  using T = Tile<D>;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int n = 0; n < TileRegs<D>::N; ++n) {
-    const int u = tid + n * kThreads;
-    const int kk = u / CH, ch = u % CH;
-    *(u32x4*)&sm.k[kk * KLD + ch * 8] = r.k[n];
-    const int kv = (u & 15) + 16 * (u / (16 * CH));
-    const int cv = (u >> 4) % CH;
-    const int p = vpos(kv);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      sm.vt[(cv * 8 + 2 * e) * VLD + p] = (uint16_t)(r.v[n][e] & 0xffffu);
-      sm.vt[(cv * 8 + 2 * e + 1) * VLD + p] = (uint16_t)(r.v[n][e] >> 16);
-    }
+  for (int n = 0; n < T::NI; ++n) {
+    const int blk = 4 * n + wave;                  // which 1 KiB slab of the sub-tile
+    const int r = T::RPI * blk + lane / T::CH;     // tile row of this lane's chunk
+    const int p = lane % T::CH;                    // physical chunk slot in the row
+    const int c = p ^ swz<D>(r);                   // logical chunk it holds
+    int key = key0 + r;
+    key = key < Lk ? key : Lk - 1;
+    const size_t off = (size_t)key * D + c * 8;
+    __builtin_amdgcn_global_load_lds((const void*)(kh + off), LDS_PTR(kdst + blk * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(vh + off), LDS_PTR(vdst + blk * 1024), 16, 0, 0);
   }
 }
 
@@ -118,20 +96,19 @@ struct Geom {
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ idx, uint16_t* __restrict__ o,
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
     float* __restrict__ part_l, Geom gm, int BH, int row_tiles, int splits, int units, float scale_log2) {
+  using T = Tile<D>;
   constexpr int KS = D / 32;   // k-steps of Q.K^T
   constexpr int DT = D / 16;   // d tiles of P.V
-  constexpr int KLD = Smem<D>::KLD, VLD = Smem<D>::VLD;
-  __shared__ Smem<D> sm;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2][2][T::BYTES];   // [stage][K|V]
 
   // XCD-aware id: hardware places consecutive workgroup ids on consecutive XCDs (round
   // robin over 8); give each XCD a contiguous range of logical units.
-  const int nwg = gridDim.x;
-  const int per_xcd = nwg >> 3;
+  const int per_xcd = gridDim.x >> 3;
   const int hw = blockIdx.x;
   const int logical = (hw & 7) * per_xcd + (hw >> 3);
   if (logical >= units) return;
@@ -180,6 +157,13 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
       qreg[qt][ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
+  // frame of each of this lane's two query rows (frame-causal mask)
+  int qframe[2] = {0, 0};
+  if (gm.F > 0) {
+    qframe[0] = (r0w + c) / gm.F;
+    qframe[1] = (r0w + 16 + c) / gm.F;
+  }
+  const int wave_first_frame = gm.F > 0 ? r0w / gm.F : 0;
 
   f32x4 oacc[DT][2];
 #pragma unroll
@@ -205,8 +189,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
   int cj, csub = 0;
   bool cA, cB;
   pop(cj, cA, cB);
-  TileRegs<D> regs;
-  if (cj != kEnd) fetch_tile<D>(regs, kh, vh, cj * gm.block, gm.Lk);
+  int stage = 0;
+  if (cj != kEnd) issue_tile<D>(smem[0][0], smem[0][1], kh, vh, cj * gm.block, gm.Lk);
   while (cj != kEnd) {
     int nj = cj, nsb = csub + 1;
     bool nA = cA, nB = cB;
@@ -214,12 +198,16 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
       nsb = 0;
       pop(nj, nA, nB);
     }
+    // this thread's loads of the current stage are done; the barrier makes every thread's
+    // loads visible and guarantees the other stage is no longer being read
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    store_tile<D>(sm, regs);
-    __syncthreads();
-    if (nj != kEnd) fetch_tile<D>(regs, kh, vh, nj * gm.block + nsb * KT, gm.Lk);
+    if (nj != kEnd)
+      issue_tile<D>(smem[stage ^ 1][0], smem[stage ^ 1][1], kh, vh, nj * gm.block + nsb * KT, gm.Lk);
     const int key0 = cj * gm.block + csub * KT;
     const bool mine = (wave_b ? cB : cA) && wave_rows;
+    const unsigned char* ks_base = smem[stage][0];
+    const unsigned char* vs_base = smem[stage][1];
     if (mine) {
       // ---- S^T = K Q^T ----
       f32x4 sacc[4][2];
@@ -229,36 +217,32 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
       for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
-          const bf16x8 a = *(const bf16x8*)&sm.k[(16 * kt + c) * KLD + 32 * ks + 8 * g];
+          const int r = 16 * kt + c;
+          const int slot = (4 * ks + g) ^ swz<D>(r);
+          const bf16x8 a = *(const bf16x8*)(ks_base + r * T::ROWB + slot * 16);
           sacc[kt][0] = mfma16(a, qreg[0][ks], sacc[kt][0]);
           sacc[kt][1] = mfma16(a, qreg[1][ks], sacc[kt][1]);
         }
       }
       // ---- masks: keys past Lk (ragged last block), frame-causal pairs in the chunk ----
-      const int key_end = key0 + KT;
-      bool need_mask = key_end > gm.Lk;
-      if (gm.F > 0 && key_end > gm.chunk0) {
-        const int last_frame = (key_end - 1 - gm.chunk0) / gm.F;
-        if (last_frame > r0w / gm.F) need_mask = true;
-      }
+      bool need_mask = key0 + KT > gm.Lk;
+      if (gm.F > 0 && key0 + KT - 1 >= gm.chunk0)
+        need_mask = need_mask || ((key0 + KT - 1 - gm.chunk0) / gm.F > wave_first_frame);
       if (need_mask) {
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          const int qrow = r0w + 16 * qt + c;
-          const int qf = gm.F > 0 ? qrow / gm.F : 0;
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-          for (int kt = 0; kt < 4; ++kt)
+          for (int i = 0; i < 4; ++i) {
+            const int key = key0 + 16 * kt + 4 * g + i;
+            const bool in_range = key < gm.Lk;
+            const int kf = (gm.F > 0 && key >= gm.chunk0) ? (key - gm.chunk0) / gm.F : -1;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int key = key0 + 16 * kt + 4 * g + i;
-              bool ok = key < gm.Lk;
-              if (gm.F > 0 && key >= gm.chunk0) ok = ok && ((key - gm.chunk0) / gm.F <= qf);
-              if (!ok) sacc[kt][qt][i] = -INFINITY;
-            }
-        }
+            for (int qt = 0; qt < 2; ++qt)
+              if (!in_range || kf > qframe[qt]) sacc[kt][qt][i] = -INFINITY;
+          }
       }
-      // ---- online softmax (base 2, scaled logits) ----
-      bf16x8 pb[2][2];
+      // ---- online softmax (base 2, scaled logits, lazy rescale) ----
+      float mt[2];
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
         float mx = -INFINITY;
@@ -268,22 +252,36 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
           for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sacc[kt][qt][i]);
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run[qt], mx * scale_log2);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = exp2f(m_run[qt] - m_use);
-        m_run[qt] = m_new;
+        mt[qt] = mx * scale_log2;
+      }
+      const bool raise0 = mt[0] > m_run[0] + kRescaleSlack;
+      const bool raise1 = mt[1] > m_run[1] + kRescaleSlack;
+      if (__any(raise0 || raise1)) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          const bool raise = qt == 0 ? raise0 : raise1;
+          const float m_new = raise ? mt[qt] : m_run[qt];
+          const float alpha = raise ? __builtin_amdgcn_exp2f(m_run[qt] - m_new) : 1.0f;
+          m_run[qt] = m_new;
+          l_run[qt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) oacc[dt][qt] *= alpha;
+        }
+      }
+      bf16x8 pb[2][2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const float m_use = (m_run[qt] == -INFINITY) ? 0.f : m_run[qt];
         float rs = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float p = exp2f(sacc[kt][qt][i] * scale_log2 - m_use);
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][qt][i], scale_log2, -m_use));
             sacc[kt][qt][i] = p;
             rs += p;
           }
-        l_run[qt] = l_run[qt] * alpha + rs;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) oacc[dt][qt] *= alpha;
+        l_run[qt] += rs;
 #pragma unroll
         for (int ks2 = 0; ks2 < 2; ++ks2) {
           u32x4 w;
@@ -294,12 +292,26 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
           pb[qt][ks2] = __builtin_bit_cast(bf16x8, w);
         }
       }
-      // ---- O^T += V^T P^T ----
+      // ---- O^T += V^T P^T : V^T operand by LDS transpose reads ----
+      // lane (g, s = c) addresses key row 32 ks2 + 16 h + 4 g + s/4 at d = 16 dt + 4 (s%4);
+      // the transpose hands it V[32 ks2 + 16 h + 4 g + j][16 dt + s], j = 0..3.
 #pragma unroll
       for (int ks2 = 0; ks2 < 2; ++ks2) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 a = *(const bf16x8*)&sm.vt[(16 * dt + c) * VLD + 32 * ks2 + 8 * g];
+          v4i16 half[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int r = 32 * ks2 + 16 * h + 4 * g + (c >> 2);
+            const int chunk = 2 * dt + ((c & 3) >> 1);
+            const int byte = r * T::ROWB + ((chunk ^ swz<D>(r)) << 4) + ((c & 1) << 3);
+            half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4i16*)(vs_base + byte));
+          }
+          const v4i16 lo = half[0], hi = half[1];
+          typedef short v8i16 __attribute__((ext_vector_type(8)));
+          const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x8 a = __builtin_bit_cast(bf16x8, a8);
           oacc[dt][0] = mfma16(a, pb[0][ks2], oacc[dt][0]);
           oacc[dt][1] = mfma16(a, pb[1][ks2], oacc[dt][1]);
         }
@@ -309,6 +321,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
     csub = nsb;
     cA = nA;
     cB = nB;
+    stage ^= 1;
   }
 
   // ---- epilogue ----
