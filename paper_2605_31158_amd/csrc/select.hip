@@ -1,16 +1,22 @@
 // Block selection on gfx950 (Sec. 3.3: pooled proxies, block relevance scores, retained set).
 //
 // Three launches per call, all on the caller's stream:
-//   pool_q        one workgroup per (head, query block): mean of the block's valid rows
-//                 -> q_bar fp32 [BH, NQ, d] (workspace).  HBM-bound streaming read.
-//   pool_k_score  one workgroup per (head, group of G historical key blocks): pools the G
-//                 blocks into LDS (never written out) and immediately scores them against
-//                 every q_bar of the head -> s fp32 [BH, NQ, M] (workspace).  The K read
-//                 dominates the selection pass; it is a single coalesced streaming pass.
-//   select_rows   one workgroup per (head, query block): softmax over the M scores, sort
-//                 by (score desc, block asc), prefix scan of the sorted probabilities to
-//                 the tau crossing (or a fixed count), merge with the forced blocks and
-//                 emit the mask row, the count and the ascending block list.
+//   pool_q        one wave per (head, query block): mean of the block's valid rows
+//                 -> q_bar fp32 [BH, NQ, d] (workspace).  Streaming read, every load of a
+//                 lane in flight at once.
+//   pool_k_score  one workgroup per (head, group of GB historical key blocks): each wave pools
+//                 whole blocks into LDS (never written out), then the workgroup scores the
+//                 GB pooled keys against every pooled query of the head with fp32 MFMA
+//                 (v_mfma_f32_16x16x4_f32) -> s fp32 [BH, NQ, M] (workspace).  The K read is
+//                 the dominant cost of selection; it is one coalesced streaming pass.
+//   select_rows   one wave per (head, query block), no workgroup barriers: softmax over the
+//                 M scores, then a radix select over the 32-bit order keys of the scores (4
+//                 passes of 8 bits, per-wave LDS histogram) that finds the score at which the
+//                 mass, accumulated from the highest score down, first reaches tau (or the
+//                 count reaches the top-k size).  Masses are 2^-32 fixed-point integers, so the
+//                 sums are exact and independent of summation order.  Equal scores at the
+//                 cutoff are taken in ascending block order.  The kept set is merged with the
+//                 forced blocks and emitted, ascending, with lane ballots: mask row, count, list.
 #include <float.h>
 #include <math.h>
 
@@ -29,108 +35,155 @@ __device__ inline void acc_bf16x8(float* a, u32x4 w) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// pooled queries
-
-template <int D>
-__global__ __launch_bounds__(kThreads) void pool_q_kernel(const uint16_t* __restrict__ q,
-                                                          float* __restrict__ qbar, int Lq, int block,
-                                                          int NQ) {
-  constexpr int CH = D / 8;             // 16-byte chunks per row
-  constexpr int RPP = kThreads / CH;    // rows one pass of the workgroup covers
-  constexpr int MAXIT = 128 / RPP;      // passes for the largest block
-  __shared__ float red[kThreads / 64][D];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i = blockIdx.x, bh = blockIdx.y;
-  const int row0 = i * block;
-  const int rows = min(block, Lq - row0);
-  const int ch = tid % CH, rg = tid / CH;
-  const uint16_t* base = q + ((size_t)bh * Lq + row0) * D + ch * 8;
-  u32x4 w[MAXIT];
+// Sums the `rows` valid rows of one block (rows x D bf16, row-major at `base`) with one wave.
+// Lane l owns 16-byte chunk l % CH of rows l / CH + RG * r; every lane's loads are issued
+// before any is consumed.  On return every lane holds the column sums of its chunk (8 floats).
+template <int D, int BLOCK>
+__device__ inline void wave_block_sum(const uint16_t* __restrict__ base, int rows, float* a) {
+  constexpr int CH = D / 8;           // chunks per row
+  constexpr int RG = 64 / CH;         // row groups per wave
+  constexpr int NL = BLOCK / RG;      // loads per lane
+  constexpr int BATCH = NL > 16 ? 16 : NL;
+  const int lane = threadIdx.x & 63;
+  const int ch = lane % CH, rg = lane / CH;
 #pragma unroll
-  for (int it = 0; it < MAXIT; ++it) {
-    const int r = rg + it * RPP;
-    if (r < rows) w[it] = *(const u32x4*)(base + (size_t)r * D);
-    else w[it] = u32x4{0u, 0u, 0u, 0u};
+  for (int e = 0; e < 8; ++e) a[e] = 0.f;
+#pragma unroll
+  for (int b0 = 0; b0 < NL; b0 += BATCH) {
+    u32x4 w[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int r = rg + RG * (b0 + u);
+      w[u] = r < rows ? *(const u32x4*)(base + (size_t)r * D + ch * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) acc_bf16x8(a, w[u]);
   }
-  float a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-  for (int it = 0; it < MAXIT; ++it) acc_bf16x8(a, w[it]);
 #pragma unroll
   for (int off = CH; off < 64; off <<= 1)
 #pragma unroll
     for (int e = 0; e < 8; ++e) a[e] += __shfl_xor(a[e], off);
-  if (lane < CH)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) red[wave][lane * 8 + e] = a[e];
-  __syncthreads();
-  if (tid < D) {
-    float s = 0.f;
-#pragma unroll
-    for (int wv = 0; wv < kThreads / 64; ++wv) s += red[wv][tid];
-    qbar[((size_t)bh * NQ + i) * D + tid] = s / (float)rows;
+}
+
+// ---------------------------------------------------------------------------
+// pooled queries: one wave per query block
+
+template <int D, int BLOCK>
+__global__ __launch_bounds__(kThreads) void pool_q_kernel(const uint16_t* __restrict__ q,
+                                                          float* __restrict__ qbar, int Lq, int NQ) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x * (kThreads / 64) + wave;
+  const int bh = blockIdx.y;
+  if (i >= NQ) return;
+  const int row0 = i * BLOCK;
+  const int rows = min(BLOCK, Lq - row0);
+  float a[8];
+  wave_block_sum<D, BLOCK>(q + ((size_t)bh * Lq + row0) * D, rows, a);
+  constexpr int CH = D / 8;
+  if (lane < CH) {
+    const float inv = 1.0f / (float)rows;
+    float* dst = qbar + ((size_t)bh * NQ + i) * D + lane * 8;
+    *(f32x4*)dst = f32x4{a[0] * inv, a[1] * inv, a[2] * inv, a[3] * inv};
+    *(f32x4*)(dst + 4) = f32x4{a[4] * inv, a[5] * inv, a[6] * inv, a[7] * inv};
   }
 }
 
 // ---------------------------------------------------------------------------
-// pooled historical keys, scored against every pooled query of the head
+// pooled historical keys, scored against every pooled query of the head (fp32 MFMA)
 
-template <int D, int G>
-__global__ __launch_bounds__(kThreads) void pool_k_score_kernel(const uint16_t* __restrict__ k,
+constexpr int kPadF = 4;        // fp32 row padding in LDS (rows 16-B aligned, banks spread)
+constexpr int kQChunk = 64;     // pooled-query rows staged in LDS at a time
+
+__device__ inline f32x4 mfma_f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+constexpr int kScoreThreads = 512;   // 8 waves: one pooled block in flight per wave
+
+template <int D, int BLOCK, int GB>
+__global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const uint16_t* __restrict__ k,
                                                                 const float* __restrict__ qbar,
-                                                                float* __restrict__ scores, int Lk,
-                                                                int block, int NQ, int h0, int M,
-                                                                float inv_sqrt_d) {
-  constexpr int CH = D / 8;        // chunks per row
-  constexpr int RG = 64 / CH;      // row groups inside one wave
-  __shared__ float kbar[G][D];
+                                                                float* __restrict__ scores, int Lk, int NQ,
+                                                                int h0, int M, float inv_sqrt_d) {
+  constexpr int LD = D + kPadF;
+  __shared__ __attribute__((aligned(16))) float kb[GB][LD];
+  __shared__ __attribute__((aligned(16))) float qb[kQChunk][LD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = blockIdx.y;
-  const int m0 = blockIdx.x * G;
-  const int gcount = min(G, M - m0);
-  const int ch = lane % CH, rg = lane / CH;
-  const int iters = block / RG;    // multiple of 8 for block 64/128 and d 64/128
-  const float inv_block = 1.0f / (float)block;
-  for (int g = wave; g < gcount; g += kThreads / 64) {
-    const int j = h0 + m0 + g;     // historical blocks are whole: no ragged rows
-    const uint16_t* base = k + ((size_t)bh * Lk + (size_t)j * block) * D + ch * 8;
-    float a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int it0 = 0; it0 < iters; it0 += 8) {
-      u32x4 w[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) w[u] = *(const u32x4*)(base + (size_t)((it0 + u) * RG + rg) * D);
-#pragma unroll
-      for (int u = 0; u < 8; ++u) acc_bf16x8(a, w[u]);
+  const int m0 = blockIdx.x * GB;
+  const int gcount = min(GB, M - m0);
+  constexpr int CH = D / 8;
+  const float inv_block = 1.0f / (float)BLOCK;
+  for (int g = wave; g < GB; g += kScoreThreads / 64) {
+    if (g < gcount) {
+      const int j = h0 + m0 + g;   // historical blocks are whole: no ragged rows
+      float a[8];
+      wave_block_sum<D, BLOCK>(k + ((size_t)bh * Lk + (size_t)j * BLOCK) * D, BLOCK, a);
+      if (lane < CH) {
+        *(f32x4*)&kb[g][lane * 8] = f32x4{a[0] * inv_block, a[1] * inv_block, a[2] * inv_block, a[3] * inv_block};
+        *(f32x4*)&kb[g][lane * 8 + 4] = f32x4{a[4] * inv_block, a[5] * inv_block, a[6] * inv_block, a[7] * inv_block};
+      }
+    } else if (lane < CH) {
+      *(f32x4*)&kb[g][lane * 8] = f32x4{0.f, 0.f, 0.f, 0.f};
+      *(f32x4*)&kb[g][lane * 8 + 4] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-#pragma unroll
-    for (int off = CH; off < 64; off <<= 1)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a[e] += __shfl_xor(a[e], off);
-    if (lane < CH)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kbar[g][lane * 8 + e] = a[e] * inv_block;
   }
-  __syncthreads();
-  const int g = tid % G;
-  if (g >= gcount) return;
-  const f32x4* kr = (const f32x4*)kbar[g];
-  for (int i = tid / G; i < NQ; i += kThreads / G) {
-    const f32x4* qr = (const f32x4*)(qbar + ((size_t)bh * NQ + i) * D);
-    float s = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < D / 4; ++c) {
-      const f32x4 x = qr[c], y = kr[c];
-      s += x[0] * y[0];
-      s += x[1] * y[1];
-      s += x[2] * y[2];
-      s += x[3] * y[3];
+  // S tile [query rows x GB] = q_bar (rows x D) . k_bar^T (D x GB), 16x16 MFMA tiles:
+  // lane l supplies A[row l%16][k l/16] and B[k l/16][col l%16]; C rows 4(l/16)+i, col l%16.
+  constexpr int CT = GB / 16;                     // column tiles
+  constexpr int NT = (kQChunk / 16) * CT;         // tiles per query chunk
+  const int c16 = lane & 15, k4 = lane >> 4;
+  for (int i0 = 0; i0 < NQ; i0 += kQChunk) {
+    __syncthreads();                              // kb complete / previous chunk consumed
+    const int nrows = min(kQChunk, NQ - i0);
+    for (int e = tid; e < kQChunk * (D / 4); e += kScoreThreads) {
+      const int r = e / (D / 4), c4 = e % (D / 4);
+      f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (r < nrows) v = *(const f32x4*)(qbar + ((size_t)bh * NQ + i0 + r) * D + c4 * 4);
+      *(f32x4*)&qb[r][c4 * 4] = v;
     }
-    scores[((size_t)bh * NQ + i) * M + m0 + g] = s * inv_sqrt_d;
+    __syncthreads();
+    for (int t = wave; t < NT; t += kScoreThreads / 64) {
+      const int rt = t / CT, ct = t % CT;
+      if (16 * rt >= nrows) continue;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+      for (int kk = 0; kk < D; kk += 4)
+        acc = mfma_f32(qb[16 * rt + c16][kk + k4], kb[16 * ct + c16][kk + k4], acc);
+      const int col = 16 * ct + c16;
+      if (col < gcount) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = 16 * rt + 4 * k4 + i;
+          if (r < nrows) scores[((size_t)bh * NQ + i0 + r) * M + m0 + col] = acc[i] * inv_sqrt_d;
+        }
+      }
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// workgroup reductions / scans (256 threads, 4 waves)
+// 64-bit lane shuffles
+
+__device__ inline uint64_t shfl_xor_u64(uint64_t x, int off) {
+  const uint32_t lo = __shfl_xor((uint32_t)x, off), hi = __shfl_xor((uint32_t)(x >> 32), off);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ inline uint64_t shfl_up_u64(uint64_t x, int off) {
+  const uint32_t lo = __shfl_up((uint32_t)x, off), hi = __shfl_up((uint32_t)(x >> 32), off);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Order key: ascending key = score descending.  -0 and +0 map to the same key.
+__device__ inline uint32_t order_key(float s) {
+  if (s == 0.0f) s = 0.0f;
+  uint32_t u = __float_as_uint(s);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);   // monotone increasing in s
+  return ~u;
+}
+
+// ---------------------------------------------------------------------------
+// wave-level helpers (one wave per query-block row: no workgroup barriers)
 
 __device__ inline float wave_max(float x) {
 #pragma unroll
@@ -142,193 +195,215 @@ __device__ inline float wave_sum(float x) {
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
   return x;
 }
-
-// Exclusive scan of one int per thread across the workgroup; *total gets the sum.
-__device__ inline int block_excl_scan(int x, int* sh, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int incl = x;
+__device__ inline uint64_t wave_sum_u64(uint64_t x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += shfl_xor_u64(x, off);
+  return x;
+}
+__device__ inline uint64_t wave_incl_scan_u64(uint64_t x) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(incl, off);
-    if (lane >= off) incl += y;
+    const uint64_t y = shfl_up_u64(x, off);
+    if (lane >= off) x += y;
   }
-  if (lane == 63) sh[wave] = incl;
-  __syncthreads();
-  int base = 0, tot = 0;
-#pragma unroll
-  for (int wv = 0; wv < kThreads / 64; ++wv) {
-    if (wv < wave) base += sh[wv];
-    tot += sh[wv];
+  return x;
+}
+__device__ inline uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
+
+// All LDS operations this wave issued have completed before the next one starts.
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Emits the forced block range [lo, hi) at list position pos (mask bytes set to 1).
+__device__ inline void emit_range(int lo, int hi, int pos, uint8_t* mask_row, int32_t* idx_row) {
+  const int lane = threadIdx.x & 63;
+  for (int j = lo + lane; j < hi; j += 64) {
+    idx_row[pos + (j - lo)] = j;
+    if (mask_row) mask_row[j] = 1;
   }
-  __syncthreads();
-  *total = tot;
-  return base + incl - x;
 }
 
-__device__ inline float block_excl_scan_f(float x, float* sh) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float incl = x;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float y = __shfl_up(incl, off);
-    if (lane >= off) incl += y;
-  }
-  if (lane == 63) sh[wave] = incl;
-  __syncthreads();
-  float base = 0.f;
-#pragma unroll
-  for (int wv = 0; wv < kThreads / 64; ++wv)
-    if (wv < wave) base += sh[wv];
-  __syncthreads();
-  return base + incl - x;
-}
+constexpr double kFix = 4294967296.0;   // 2^32 fixed-point scale of the mass
 
-// Sort key: ascending key order = score descending, then candidate index ascending.
-__device__ inline uint64_t sort_key(float s, int m) {
-  if (s == 0.0f) s = 0.0f;                      // -0 and +0 compare equal
-  uint32_t u = __float_as_uint(s);
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);   // monotone in s
-  return ((uint64_t)(~u) << 32) | (uint32_t)m;
-}
-
-// Writes the mask row (optional), the ascending kept list and its length from the
-// per-block flags in LDS.
-__device__ inline void emit_row(const uint8_t* flag, int NK, uint8_t* mask_row, int32_t* idx_row,
-                                int32_t* count, int* sh_i) {
-  const int tid = threadIdx.x;
-  const int per = (NK + kThreads - 1) / kThreads;
-  const int lo = min(tid * per, NK), hi = min(lo + per, NK);
-  int cnt = 0;
-  for (int j = lo; j < hi; ++j) cnt += flag[j];
-  int total;
-  int pos = block_excl_scan(cnt, sh_i, &total);
-  for (int j = lo; j < hi; ++j)
-    if (flag[j]) idx_row[pos++] = j;
-  if (tid == 0) *count = total;
-  if (mask_row)
-    for (int j = tid; j < NK; j += kThreads) mask_row[j] = flag[j];
-}
-
+// One wave per (head, query block).  Lane l holds candidates m = l + 64 j, j < NPER.
+template <int NPER>
 __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __restrict__ scores, int NQ,
-                                                               int NK, int M, int P, int h0, int h1,
-                                                               float tau, int keep_fixed,
-                                                               uint8_t* __restrict__ mask,
+                                                               int NK, int M, int h0, int h1, float tau,
+                                                               int keep_fixed, uint8_t* __restrict__ mask,
                                                                int32_t* __restrict__ counts,
                                                                int32_t* __restrict__ idx) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  uint64_t* keys = (uint64_t*)smem;                 // [P]
-  float* prob = (float*)(keys + P);                 // [P], indexed by candidate
-  uint8_t* flag = (uint8_t*)(prob + P);             // [NK]
-  __shared__ float sh_f[kThreads / 64];
-  __shared__ int sh_i[kThreads / 64];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i = blockIdx.x, bh = blockIdx.y;
+  __shared__ uint64_t hist_all[kThreads / 64][256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x * (kThreads / 64) + wave;
+  const int bh = blockIdx.y;
+  if (i >= NQ) return;
+  uint64_t* hist = hist_all[wave];
   const size_t row = (size_t)bh * NQ + i;
   const float* s = scores + row * (size_t)M;
+  uint8_t* mask_row = mask ? mask + row * (size_t)NK : nullptr;
+  int32_t* idx_row = idx + row * (size_t)NK;
 
-  for (int j = tid; j < NK; j += kThreads) flag[j] = (j < h0 || j >= h1) ? 1 : 0;
-  if (M > 0) {
-    // softmax over the M candidates
-    float mx = -FLT_MAX;
-    for (int m = tid; m < M; m += kThreads) mx = fmaxf(mx, s[m]);
-    mx = wave_max(mx);
-    if (lane == 0) sh_f[wave] = mx;
-    __syncthreads();
-    mx = sh_f[0];
+  float sv[NPER];
+  uint32_t w[NPER];
 #pragma unroll
-    for (int wv = 1; wv < kThreads / 64; ++wv) mx = fmaxf(mx, sh_f[wv]);
-    __syncthreads();
-    float sum = 0.f;
-    for (int m = tid; m < M; m += kThreads) {
-      const float e = expf(s[m] - mx);
-      prob[m] = e;
-      sum += e;
-    }
-    sum = wave_sum(sum);
-    if (lane == 0) sh_f[wave] = sum;
-    __syncthreads();
-    sum = 0.f;
-#pragma unroll
-    for (int wv = 0; wv < kThreads / 64; ++wv) sum += sh_f[wv];
-    for (int m = tid; m < P; m += kThreads) {
-      if (m < M) {
-        prob[m] = prob[m] / sum;
-        keys[m] = sort_key(s[m], m);
-      } else {
-        keys[m] = ~(uint64_t)0;
-      }
-    }
-    __syncthreads();
-    // bitonic sort, ascending keys
-    for (int kk = 2; kk <= P; kk <<= 1) {
-      for (int jj = kk >> 1; jj > 0; jj >>= 1) {
-        for (int t = tid; t < (P >> 1); t += kThreads) {
-          const int a = (t / jj) * 2 * jj + (t % jj);
-          const int b = a + jj;
-          const uint64_t x = keys[a], y = keys[b];
-          const bool up = (a & kk) == 0;
-          if ((x > y) == up) {
-            keys[a] = y;
-            keys[b] = x;
-          }
-        }
-        __syncthreads();
-      }
-    }
-    int kstar;
+  for (int j = 0; j < NPER; ++j) {
+    const int m = lane + 64 * j;
+    sv[j] = m < M ? s[m] : -FLT_MAX;
+  }
+  // mode: keep all / keep none / select
+  bool keep_all = keep_fixed < 0 ? tau >= 1.0f : keep_fixed >= M;
+  uint64_t target = 0;
+  if (!keep_all) {
     if (keep_fixed >= 0) {
-      kstar = min(keep_fixed, M);
-    } else if (tau >= 1.0f) {
-      kstar = M;
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) w[j] = (lane + 64 * j < M) ? 1u : 0u;
+      target = (uint64_t)keep_fixed;
     } else {
-      // cumulative mass over ranks; first rank whose inclusive sum reaches tau
-      const int per = (M + kThreads - 1) / kThreads;
-      const int lo = min(tid * per, M), hi = min(lo + per, M);
-      float local = 0.f;
-      for (int r = lo; r < hi; ++r) local += prob[(uint32_t)keys[r]];
-      float run = block_excl_scan_f(local, sh_f);
-      int first = M;
-      for (int r = lo; r < hi; ++r) {
-        run += prob[(uint32_t)keys[r]];
-        if (run >= tau) {
-          first = r;
+      float mx = -FLT_MAX;
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) mx = fmaxf(mx, sv[j]);
+      mx = wave_max(mx);
+      float e[NPER];
+      float sum = 0.f;
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) {
+        e[j] = (lane + 64 * j < M) ? expf(sv[j] - mx) : 0.f;
+        sum += e[j];
+      }
+      sum = wave_sum(sum);
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) {
+        const double f = (double)(e[j] / sum) * kFix;
+        w[j] = f >= 4294967295.0 ? 0xffffffffu : (uint32_t)f;
+      }
+      target = (uint64_t)((double)tau * kFix);
+      if (target == 0) target = 1;     // any tau > 0 keeps at least the top candidate
+    }
+    uint64_t wl = 0;
+#pragma unroll
+    for (int j = 0; j < NPER; ++j) wl += w[j];
+    if (wave_sum_u64(wl) < target) keep_all = true;   // the mass / count never reaches the target
+  }
+  // cutoff: smallest order key u* whose inclusive weight reaches the target (radix select,
+  // 4 passes of 8 bits over a per-wave 256-bin histogram), then equal keys by block index
+  uint32_t ustar = 0xffffffffu;
+  int mstar = 0x7fffffff;
+  const bool none = !keep_all && target == 0;
+  if (!keep_all && !none) {
+    uint32_t prefix = 0;
+    uint64_t before = 0;
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) hist[4 * lane + t] = 0;
+      wave_lds_sync();
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) {
+        const uint32_t uk = order_key(sv[j]);
+        const bool in = w[j] != 0 && (pass == 0 || (uk >> (shift + 8)) == prefix);
+        if (in) atomicAdd((unsigned long long*)&hist[(uk >> shift) & 255u], (unsigned long long)w[j]);
+      }
+      wave_lds_sync();
+      uint64_t b4[4];
+      uint64_t loc = 0;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        loc += hist[4 * lane + t];
+        b4[t] = loc;
+      }
+      const uint64_t excl = wave_incl_scan_u64(loc) - loc;
+      int hit = -1;
+#pragma unroll
+      for (int t = 3; t >= 0; --t)
+        if (before + excl + b4[t] >= target) hit = t;
+      const unsigned long long bal = __ballot(hit >= 0);
+      const int first = __ffsll(bal) - 1;              // lane holding the crossing bin
+      const uint64_t below = before + excl + (hit > 0 ? b4[hit > 0 ? hit - 1 : 0] : 0);
+      const int bin = 4 * lane + hit;
+      prefix = (prefix << 8) | (uint32_t)__shfl(bin, first);
+      before = ((uint64_t)(uint32_t)__shfl((uint32_t)(below >> 32), first) << 32) |
+               (uint32_t)__shfl((uint32_t)below, first);
+    }
+    ustar = prefix;
+    int ntie = 0;
+#pragma unroll
+    for (int j = 0; j < NPER; ++j) ntie += (w[j] != 0 && order_key(sv[j]) == ustar) ? 1 : 0;
+    if ((int)wave_sum((float)ntie) > 1) {
+      // equal scores at the cutoff: take them in ascending block order until the target
+      uint64_t base = before;
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) {
+        const uint64_t wt = (w[j] != 0 && order_key(sv[j]) == ustar) ? w[j] : 0;
+        const uint64_t incl = wave_incl_scan_u64(wt);
+        const bool cross = wt != 0 && base + incl >= target && base + incl - wt < target;
+        const unsigned long long bal = __ballot(cross);
+        if (bal) {
+          mstar = 64 * j + __ffsll(bal) - 1;
           break;
         }
+        base += (uint64_t)__shfl((uint32_t)incl, 63) | ((uint64_t)(uint32_t)__shfl((uint32_t)(incl >> 32), 63) << 32);
       }
-      // workgroup minimum
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) first = min(first, __shfl_xor(first, off));
-      if (lane == 0) sh_i[wave] = first;
-      __syncthreads();
-      first = sh_i[0];
-#pragma unroll
-      for (int wv = 1; wv < kThreads / 64; ++wv) first = min(first, sh_i[wv]);
-      __syncthreads();
-      kstar = (first < M) ? first + 1 : M;
     }
-    for (int r = tid; r < kstar; r += kThreads) flag[h0 + (int)(uint32_t)keys[r]] = 1;
   }
-  __syncthreads();
-  emit_row(flag, NK, mask ? mask + row * (size_t)NK : nullptr, idx + row * (size_t)NK, counts + row, sh_i);
+  // emit: forced head, kept historical blocks (ascending), forced tail
+  emit_range(0, h0, 0, mask_row, idx_row);
+  int pos = h0;
+#pragma unroll
+  for (int j = 0; j < NPER; ++j) {
+    const int m = lane + 64 * j;
+    bool kept = false;
+    if (m < M) {
+      if (keep_all) kept = true;
+      else if (!none) {
+        const uint32_t uk = order_key(sv[j]);
+        kept = w[j] != 0 && (uk < ustar || (uk == ustar && m <= mstar));
+      }
+      if (mask_row) mask_row[h0 + m] = kept ? 1 : 0;
+    }
+    const unsigned long long bal = __ballot(kept);
+    if (kept) idx_row[pos + __popcll(bal & lanes_below(lane))] = h0 + m;
+    pos += __popcll(bal);
+  }
+  emit_range(h1, NK, pos, mask_row, idx_row);
+  if (lane == 0) counts[row] = pos + (NK - h1);
 }
 
+// One wave per (head, query block): compacts a mask row into the ascending list.
 __global__ __launch_bounds__(kThreads) void mask_to_list_kernel(const uint8_t* __restrict__ mask, int NQ,
                                                                 int NK, int32_t* __restrict__ counts,
                                                                 int32_t* __restrict__ idx) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  uint8_t* flag = (uint8_t*)smem;
-  __shared__ int sh_i[kThreads / 64];
-  const size_t row = (size_t)blockIdx.y * NQ + blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x * (kThreads / 64) + wave;
+  if (i >= NQ) return;
+  const size_t row = (size_t)blockIdx.y * NQ + i;
   const uint8_t* mr = mask + row * (size_t)NK;
-  for (int j = threadIdx.x; j < NK; j += kThreads) flag[j] = mr[j] ? 1 : 0;
-  __syncthreads();
-  emit_row(flag, NK, nullptr, idx + row * (size_t)NK, counts + row, sh_i);
+  int32_t* idx_row = idx + row * (size_t)NK;
+  int pos = 0;
+  for (int j0 = 0; j0 < NK; j0 += 64) {
+    const int j = j0 + lane;
+    const bool kept = j < NK && mr[j] != 0;
+    const unsigned long long bal = __ballot(kept);
+    if (kept) idx_row[pos + __popcll(bal & lanes_below(lane))] = j;
+    pos += __popcll(bal);
+  }
+  if (lane == 0) counts[row] = pos;
 }
 
-int next_pow2(int x) {
-  int p = 2;
-  while (p < x) p <<= 1;
-  return p;
+template <int D, int BLOCK>
+void launch_pools(const Dims& dm, const void* q, const void* k, float* qbar, float* scores, hipStream_t st) {
+  const float inv_sqrt_d = 1.0f / sqrtf((float)dm.d);
+  hipLaunchKernelGGL((pool_q_kernel<D, BLOCK>), dim3(ceil_div(dm.NQ, kThreads / 64), dm.BH), dim3(kThreads), 0,
+                     st, (const uint16_t*)q, qbar, dm.Lq, dm.NQ);
+  // 32 key blocks per workgroup when that still gives >= 1 workgroup per CU, else 16
+  if ((int64_t)ceil_div(dm.M, 32) * dm.BH >= 256)
+    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 32>), dim3(ceil_div(dm.M, 32), dm.BH), dim3(kScoreThreads),
+                       0, st, (const uint16_t*)k, qbar, scores, dm.Lk, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
+  else
+    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 16>), dim3(ceil_div(dm.M, 16), dm.BH), dim3(kScoreThreads),
+                       0, st, (const uint16_t*)k, qbar, scores, dm.Lk, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
 }
 
 }  // namespace
@@ -337,34 +412,28 @@ hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau
                          uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st) {
   float* qbar = (float*)ws;
   float* scores = (float*)((char*)ws + align256((size_t)dm.BH * dm.NQ * dm.d * sizeof(float)));
-  const float inv_sqrt_d = 1.0f / sqrtf((float)dm.d);
-  constexpr int G = 8;
   if (dm.M > 0) {
-    dim3 gq(dm.NQ, dm.BH), gk(ceil_div(dm.M, G), dm.BH);
-    if (dm.d == 128) {
-      hipLaunchKernelGGL(pool_q_kernel<128>, gq, dim3(kThreads), 0, st, (const uint16_t*)q, qbar, dm.Lq,
-                         dm.block, dm.NQ);
-      hipLaunchKernelGGL((pool_k_score_kernel<128, G>), gk, dim3(kThreads), 0, st, (const uint16_t*)k, qbar,
-                         scores, dm.Lk, dm.block, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
-    } else {
-      hipLaunchKernelGGL(pool_q_kernel<64>, gq, dim3(kThreads), 0, st, (const uint16_t*)q, qbar, dm.Lq,
-                         dm.block, dm.NQ);
-      hipLaunchKernelGGL((pool_k_score_kernel<64, G>), gk, dim3(kThreads), 0, st, (const uint16_t*)k, qbar,
-                         scores, dm.Lk, dm.block, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
-    }
+    if (dm.d == 128 && dm.block == 64) launch_pools<128, 64>(dm, q, k, qbar, scores, st);
+    else if (dm.d == 128) launch_pools<128, 128>(dm, q, k, qbar, scores, st);
+    else if (dm.block == 64) launch_pools<64, 64>(dm, q, k, qbar, scores, st);
+    else launch_pools<64, 128>(dm, q, k, qbar, scores, st);
   }
-  const int P = dm.M > 0 ? next_pow2(dm.M) : 0;
-  const size_t shmem = (size_t)P * (sizeof(uint64_t) + sizeof(float)) + (size_t)((dm.NK + 15) & ~15);
-  hipLaunchKernelGGL(select_rows_kernel, dim3(dm.NQ, dm.BH), dim3(kThreads), shmem, st, scores, dm.NQ, dm.NK,
-                     dm.M, P, dm.h0, dm.h1, tau, keep_fixed, mask, counts, idx);
+  const dim3 grid(ceil_div(dm.NQ, kThreads / 64), dm.BH);
+#define LA_SELECT(NPER)                                                                                      \
+  hipLaunchKernelGGL(select_rows_kernel<NPER>, grid, dim3(kThreads), 0, st, scores, dm.NQ, dm.NK, dm.M, dm.h0, \
+                     dm.h1, tau, keep_fixed, mask, counts, idx)
+  if (dm.M <= 64 * 4) LA_SELECT(4);
+  else if (dm.M <= 64 * 16) LA_SELECT(16);
+  else if (dm.M <= 64 * 32) LA_SELECT(32);
+  else LA_SELECT(64);
+#undef LA_SELECT
   return hipGetLastError();
 }
 
 hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,
                                hipStream_t st) {
-  const size_t shmem = (size_t)((dm.NK + 15) & ~15);
-  hipLaunchKernelGGL(mask_to_list_kernel, dim3(dm.NQ, dm.BH), dim3(kThreads), shmem, st, mask, dm.NQ, dm.NK,
-                     counts, idx);
+  hipLaunchKernelGGL(mask_to_list_kernel, dim3(ceil_div(dm.NQ, kThreads / 64), dm.BH), dim3(kThreads), 0, st,
+                     mask, dm.NQ, dm.NK, counts, idx);
   return hipGetLastError();
 }
 

