@@ -8,23 +8,25 @@
 //     order (a two-pointer merge over the sorted lists).  Every kept block is staged once in
 //     LDS and consumed by the waves whose query block kept it; the other waves only help
 //     load.  Forced (chunk) blocks are kept by every query block, so most tiles are shared.
-//   * Key blocks are consumed in 64-key sub-tiles, staged by asynchronous direct-to-LDS
+//   * Key blocks are consumed in 64-key sub-tiles, staged by asynchronous buffer-to-LDS
 //     16-byte loads into a double buffer: sub-tile t+1 streams in while sub-tile t is
-//     multiplied, with one workgroup barrier per sub-tile.
+//     multiplied, with one workgroup barrier per sub-tile.  The buffer descriptor of a
+//     sub-tile ends at Lk, so the ragged last block reads zeros past the end.
 //   * Workgroup ids are remapped so that each XCD (each L2) works on consecutive (head,
 //     row tile) units: the kept K/V blocks of a head stay hot in one XCD's L2.
 //   * Few work units (small problems) split the key-block range across workgroups; the
 //     partial (O, m, l) are merged by attn_combine (log-sum-exp merge).
 //
 // Per wave and 64-key sub-tile (d = 128):
-//   S^T (64 keys x 32 queries) = K_tile (64 x d) . Q^T       32 x v_mfma_f32_16x16x32_bf16
+//   S^T (64 keys x 32 queries) = K_tile (64 x d) . Q^T       16 x v_mfma_f32_32x32x16_bf16
 //   online softmax over keys (fp32, base 2; the running max is only raised when a tile's
 //   max exceeds it by more than 2^8, so most tiles skip the rescale of O)
-//   O^T (d x 32) += V^T (d x 64) . P^T (64 x 32)              32 x v_mfma_f32_16x16x32_bf16
-// S^T is computed transposed so that its accumulator layout (each lane holds 4 consecutive
-// keys of one query column) is directly the B operand of the P.V product.  K and V tiles are
-// row-major in LDS with a per-row XOR swizzle of the 16-byte chunks (conflict-free operand
-// reads); the V^T operand is read with the LDS transpose load ds_read_b64_tr_b16.
+//   O^T (d x 32) += V^T (d x 64) . P^T (64 x 32)              16 x v_mfma_f32_32x32x16_bf16
+// S^T is computed transposed so that its accumulator layout (each lane holds 16 keys of one
+// query column) is, 8 values at a time, directly the B operand of the P.V product.  K and V
+// tiles are row-major in LDS with padded rows; every operand read is a lane base address
+// plus a compile-time offset.  The V^T operand is read with the LDS transpose load
+// ds_read_b64_tr_b16 (two per MFMA).
 #include <math.h>
 
 #include "la_internal.h"
@@ -40,10 +42,12 @@ constexpr int kEnd = 0x7fffffff;
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the running max is raised
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
-#define LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+#define LDS_AS __attribute__((address_space(3)))
 
-__device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+__device__ inline f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
@@ -51,43 +55,58 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-// Per-row XOR swizzle of the 16-byte chunks of a tile row.  Chosen so that (a) the 16 rows
-// one MFMA operand read touches map a fixed chunk to 16 distinct bank groups and (b) the
-// transpose reads of V (8 rows x 2 adjacent chunks per half-wave) are conflict-free.
-template <int D>
-__device__ inline int swz(int r) {
-  if constexpr (D == 128) return ((r & 7) << 1) | ((r >> 3) & 1);
-  else return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
-}
-
+// LDS layout of one stage: a K tile and a V tile, each 64 key rows of D bf16, row-major with
+// padded rows.  K rows are padded to D*2 + 16 bytes: the 32 key rows an MFMA operand read
+// touches (16 per LDS cycle) start in distinct 16-byte bank groups.  V rows are padded to
+// D*2 + 64 bytes: a transpose read touches 4 rows x 64 contiguous bytes per half-wave, which
+// then cover all 64 banks exactly once.
 template <int D>
 struct Tile {
-  static constexpr int CH = D / 8;                 // 16-byte chunks per row
-  static constexpr int ROWB = D * 2;               // bytes per row
-  static constexpr int RPI = 64 / CH;              // rows one wave-wide 1 KiB load covers
-  static constexpr int NI = KT / (RPI * 4);        // loads per thread per matrix per sub-tile
-  static constexpr int BYTES = KT * ROWB;          // one matrix sub-tile
+  static constexpr int KSTRIDE = D * 2 + 16;
+  static constexpr int VSTRIDE = D * 2 + 64;
+  static constexpr int KSLOTS = KSTRIDE / 16;          // 16-byte slots per K row
+  static constexpr int VSLOTS = VSTRIDE / 16;
+  static constexpr int KBYTES = KT * KSTRIDE;
+  static constexpr int VBYTES = KT * VSTRIDE;
+  static constexpr int KINST = KT * KSLOTS / 64;       // wave-wide 1 KiB loads per K tile
+  static constexpr int VINST = KT * VSLOTS / 64;
+  static constexpr int KPER = (KINST + 3) / 4;         // per wave (4 waves)
+  static constexpr int VPER = (VINST + 3) / 4;
+  static constexpr int STAGE = KBYTES + VBYTES;
 };
 
-// Issues the direct-to-LDS loads of one K and one V sub-tile (64 keys from key0; rows past
-// Lk re-read row Lk-1, their logits are masked).  Lane l of a wave-wide load lands at
-// dst + 16 l, so the swizzle is applied by choosing which global chunk each lane fetches.
+// Global byte offset (inside a tile of 64 rows) that lane `lane` of load `n` fetches so that it
+// lands at LDS slot 64 n + lane of a padded layout with `slots` slots per row; padding slots get
+// an offset past any buffer (they read as zero).
 template <int D>
-__device__ inline void issue_tile(unsigned char* kdst, unsigned char* vdst, const uint16_t* __restrict__ kh,
-                                  const uint16_t* __restrict__ vh, int key0, int Lk) {
+__device__ inline uint32_t slot_offset(int n, int lane, int slots) {
+  const int slot = 64 * n + lane;
+  const int row = slot / slots, chunk = slot % slots;
+  return chunk < D / 8 ? (uint32_t)(row * D * 2 + chunk * 16) : 0x7fffffffu;
+}
+
+// Issues this wave's buffer-to-LDS loads of one 64-key sub-tile (K and V) into `stage`.
+// The buffer descriptors start at the sub-tile and end at Lk, so rows past Lk (and the
+// padding slots, whose offsets lie past any buffer) read as zero.
+template <int D>
+__device__ inline void issue_tile(unsigned char* stage, const uint16_t* kh, const uint16_t* vh, int key0,
+                                  int Lk, const uint32_t* koff, const uint32_t* voff, int wave) {
   using T = Tile<D>;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // a sub-tile may start at or past Lk (second half of a ragged 128-key block): no valid rows
+  const uint32_t nrec = key0 < Lk ? (uint32_t)(Lk - key0) * (uint32_t)(D * 2) : 0u;
+  const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc((void*)(kh + (size_t)key0 * D), 0, nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc((void*)(vh + (size_t)key0 * D), 0, nrec, 0x00020000);
 #pragma unroll
-  for (int n = 0; n < T::NI; ++n) {
-    const int blk = 4 * n + wave;                  // which 1 KiB slab of the sub-tile
-    const int r = T::RPI * blk + lane / T::CH;     // tile row of this lane's chunk
-    const int p = lane % T::CH;                    // physical chunk slot in the row
-    const int c = p ^ swz<D>(r);                   // logical chunk it holds
-    int key = key0 + r;
-    key = key < Lk ? key : Lk - 1;
-    const size_t off = (size_t)key * D + c * 8;
-    __builtin_amdgcn_global_load_lds((const void*)(kh + off), LDS_PTR(kdst + blk * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(vh + off), LDS_PTR(vdst + blk * 1024), 16, 0, 0);
+  for (int u = 0; u < T::KPER; ++u) {
+    const int n = wave + 4 * u;
+    if (T::KINST % 4 == 0 || n < T::KINST)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (LDS_AS void*)(stage + 1024 * n), 16, koff[u], 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < T::VPER; ++u) {
+    const int n = wave + 4 * u;
+    if (T::VINST % 4 == 0 || n < T::VINST)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (LDS_AS void*)(stage + T::KBYTES + 1024 * n), 16, voff[u], 0, 0, 0);
   }
 }
 
@@ -102,9 +121,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
     float* __restrict__ part_l, Geom gm, int BH, int row_tiles, int splits, int units, float scale_log2) {
   using T = Tile<D>;
-  constexpr int KS = D / 32;   // k-steps of Q.K^T
-  constexpr int DT = D / 16;   // d tiles of P.V
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[2][2][T::BYTES];   // [stage][K|V]
+  constexpr int KS = D / 16;   // k-steps of Q.K^T (32x32x16)
+  constexpr int DT = D / 32;   // d tiles of P.V
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * T::STAGE];
 
   // XCD-aware id: hardware places consecutive workgroup ids on consecutive XCDs (round
   // robin over 8); give each XCD a contiguous range of logical units.
@@ -117,7 +136,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int bh = logical / (splits * row_tiles);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int c = lane & 15, g = lane >> 4;
+  const int c32 = lane & 31, h = lane >> 5;
   const int row_base = rt * QR;
   const int r0w = row_base + wave * QW;                 // first query row of this wave
   const bool two = (gm.block == 64);
@@ -145,31 +164,45 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const uint16_t* kh = k + (size_t)bh * gm.Lk * D;
   const uint16_t* vh = v + (size_t)bh * gm.Lk * D;
 
-  // Q^T operand: lane holds Q[row r0w + 16 qt + c][32 ks + 8 g .. + 7]
-  bf16x8 qreg[2][KS];
+  // lane-constant global offsets of this wave's tile loads
+  uint32_t koff[T::KPER], voff[T::VPER];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    const int row = r0w + 16 * qt + c;
+  for (int u = 0; u < T::KPER; ++u) {
+    const int n = wave + 4 * u;
+    koff[u] = n < T::KINST ? slot_offset<D>(n, lane, T::KSLOTS) : 0x7fffffffu;
+  }
+#pragma unroll
+  for (int u = 0; u < T::VPER; ++u) {
+    const int n = wave + 4 * u;
+    voff[u] = n < T::VINST ? slot_offset<D>(n, lane, T::VSLOTS) : 0x7fffffffu;
+  }
+  // Q^T operand (32x32x16 B): lane holds Q[row r0w + l%32][16 ks + 8 (l/32) .. + 7]
+  bf16x8 qreg[KS];
+  {
+    const int row = r0w + c32;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       u32x4 w = u32x4{0u, 0u, 0u, 0u};
-      if (row < gm.Lq) w = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 32 * ks + 8 * g);
-      qreg[qt][ks] = __builtin_bit_cast(bf16x8, w);
+      if (row < gm.Lq) w = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 16 * ks + 8 * h);
+      qreg[ks] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  // frame of each of this lane's two query rows (frame-causal mask)
-  int qframe[2] = {0, 0};
-  if (gm.F > 0) {
-    qframe[0] = (r0w + c) / gm.F;
-    qframe[1] = (r0w + 16 + c) / gm.F;
-  }
+  const int qframe = gm.F > 0 ? (r0w + c32) / gm.F : 0;
   const int wave_first_frame = gm.F > 0 ? r0w / gm.F : 0;
 
-  f32x4 oacc[DT][2];
+  f32x16 oacc[DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) oacc[dt][0] = oacc[dt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+
+  // LDS read bases (bytes within a stage): K operand row l%32, d offset 8 (l/32);
+  // V^T transpose read, 16-lane group G = l/16, lane i = l%16: row 4 (l/32) + i/4 of the
+  // 16-key step, d = 16 (G%2) + 4 (i%4).
+  const int kbase = c32 * T::KSTRIDE + 16 * h;
+  const int vbase = T::KBYTES + (4 * h + ((lane & 15) >> 2)) * T::VSTRIDE + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
 
   const int nsub = gm.block / KT;
   // Merged walk over the two ascending lists: pop() yields the next kept block and which
@@ -190,7 +223,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   bool cA, cB;
   pop(cj, cA, cB);
   int stage = 0;
-  if (cj != kEnd) issue_tile<D>(smem[0][0], smem[0][1], kh, vh, cj * gm.block, gm.Lk);
+  if (cj != kEnd) issue_tile<D>(smem, kh, vh, cj * gm.block, gm.Lk, koff, voff, wave);
   while (cj != kEnd) {
     int nj = cj, nsb = csub + 1;
     bool nA = cA, nB = cB;
@@ -203,117 +236,89 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (nj != kEnd)
-      issue_tile<D>(smem[stage ^ 1][0], smem[stage ^ 1][1], kh, vh, nj * gm.block + nsb * KT, gm.Lk);
+      issue_tile<D>(smem + (stage ^ 1) * T::STAGE, kh, vh, nj * gm.block + nsb * KT, gm.Lk, koff, voff, wave);
     const int key0 = cj * gm.block + csub * KT;
     const bool mine = (wave_b ? cB : cA) && wave_rows;
-    const unsigned char* ks_base = smem[stage][0];
-    const unsigned char* vs_base = smem[stage][1];
+    const unsigned char* sb = smem + stage * T::STAGE;
     if (mine) {
-      // ---- S^T = K Q^T ----
-      f32x4 sacc[4][2];
+      // ---- S^T = K Q^T : two 32x32 tiles over keys 0..31, 32..63 ----
+      f32x16 sacc[2];
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) sacc[kt][0] = sacc[kt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sacc[kt][i] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          const int r = 16 * kt + c;
-          const int slot = (4 * ks + g) ^ swz<D>(r);
-          const bf16x8 a = *(const bf16x8*)(ks_base + r * T::ROWB + slot * 16);
-          sacc[kt][0] = mfma16(a, qreg[0][ks], sacc[kt][0]);
-          sacc[kt][1] = mfma16(a, qreg[1][ks], sacc[kt][1]);
+        for (int kt = 0; kt < 2; ++kt) {
+          const bf16x8 a = *(const bf16x8*)(sb + kbase + kt * 32 * T::KSTRIDE + 32 * ks);
+          sacc[kt] = mfma32(a, qreg[ks], sacc[kt]);
         }
       }
       // ---- masks: keys past Lk (ragged last block), frame-causal pairs in the chunk ----
+      // lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of query r0w + l%32
       bool need_mask = key0 + KT > gm.Lk;
       if (gm.F > 0 && key0 + KT - 1 >= gm.chunk0)
         need_mask = need_mask || ((key0 + KT - 1 - gm.chunk0) / gm.F > wave_first_frame);
       if (need_mask) {
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = key0 + 16 * kt + 4 * g + i;
-            const bool in_range = key < gm.Lk;
-            const int kf = (gm.F > 0 && key >= gm.chunk0) ? (key - gm.chunk0) / gm.F : -1;
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt)
-              if (!in_range || kf > qframe[qt]) sacc[kt][qt][i] = -INFINITY;
+          for (int i = 0; i < 16; ++i) {
+            const int key = key0 + 32 * kt + 8 * (i >> 2) + 4 * h + (i & 3);
+            bool ok = key < gm.Lk;
+            if (gm.F > 0 && key >= gm.chunk0) ok = ok && ((key - gm.chunk0) / gm.F <= qframe);
+            if (!ok) sacc[kt][i] = -INFINITY;
           }
       }
       // ---- online softmax (base 2, scaled logits, lazy rescale) ----
-      float mt[2];
+      float mx = -INFINITY;
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        float mx = -INFINITY;
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mt = mx * scale_log2;
+      const bool raise = mt > m_run + kRescaleSlack;
+      if (__any(raise)) {
+        const float m_new = raise ? mt : m_run;
+        const float alpha = raise ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+        m_run = m_new;
+        l_run *= alpha;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sacc[kt][qt][i]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        mt[qt] = mx * scale_log2;
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
       }
-      const bool raise0 = mt[0] > m_run[0] + kRescaleSlack;
-      const bool raise1 = mt[1] > m_run[1] + kRescaleSlack;
-      if (__any(raise0 || raise1)) {
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+      float rs = 0.f;
+      bf16x8 pb[4];
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          const bool raise = qt == 0 ? raise0 : raise1;
-          const float m_new = raise ? mt[qt] : m_run[qt];
-          const float alpha = raise ? __builtin_amdgcn_exp2f(m_run[qt] - m_new) : 1.0f;
-          m_run[qt] = m_new;
-          l_run[qt] *= alpha;
+      for (int s = 0; s < 4; ++s) {
+        float p[8];
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) oacc[dt][qt] *= alpha;
+        for (int j = 0; j < 8; ++j) {
+          p[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s >> 1][8 * (s & 1) + j], scale_log2, -m_use));
+          rs += p[j];
         }
+        u32x4 w;
+        w[0] = pack_bf16x2(p[0], p[1]);
+        w[1] = pack_bf16x2(p[2], p[3]);
+        w[2] = pack_bf16x2(p[4], p[5]);
+        w[3] = pack_bf16x2(p[6], p[7]);
+        pb[s] = __builtin_bit_cast(bf16x8, w);
       }
-      bf16x8 pb[2][2];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        const float m_use = (m_run[qt] == -INFINITY) ? 0.f : m_run[qt];
-        float rs = 0.f;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kt][qt][i], scale_log2, -m_use));
-            sacc[kt][qt][i] = p;
-            rs += p;
-          }
-        l_run[qt] += rs;
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-          u32x4 w;
-          w[0] = pack_bf16x2(sacc[2 * ks2][qt][0], sacc[2 * ks2][qt][1]);
-          w[1] = pack_bf16x2(sacc[2 * ks2][qt][2], sacc[2 * ks2][qt][3]);
-          w[2] = pack_bf16x2(sacc[2 * ks2 + 1][qt][0], sacc[2 * ks2 + 1][qt][1]);
-          w[3] = pack_bf16x2(sacc[2 * ks2 + 1][qt][2], sacc[2 * ks2 + 1][qt][3]);
-          pb[qt][ks2] = __builtin_bit_cast(bf16x8, w);
-        }
-      }
+      l_run += rs;
       // ---- O^T += V^T P^T : V^T operand by LDS transpose reads ----
-      // lane (g, s = c) addresses key row 32 ks2 + 16 h + 4 g + s/4 at d = 16 dt + 4 (s%4);
-      // the transpose hands it V[32 ks2 + 16 h + 4 g + j][16 dt + s], j = 0..3.
 #pragma unroll
-      for (int ks2 = 0; ks2 < 2; ++ks2) {
+      for (int s = 0; s < 4; ++s) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          v4i16 half[2];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int r = 32 * ks2 + 16 * h + 4 * g + (c >> 2);
-            const int chunk = 2 * dt + ((c & 3) >> 1);
-            const int byte = r * T::ROWB + ((chunk ^ swz<D>(r)) << 4) + ((c & 1) << 3);
-            half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) v4i16*)(vs_base + byte));
-          }
-          const v4i16 lo = half[0], hi = half[1];
-          typedef short v8i16 __attribute__((ext_vector_type(8)));
+          const unsigned char* va = sb + vbase + (16 * s) * T::VSTRIDE + 64 * dt;
+          const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va));
+          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va + 8 * T::VSTRIDE));
           const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          const bf16x8 a = __builtin_bit_cast(bf16x8, a8);
-          oacc[dt][0] = mfma16(a, pb[0][ks2], oacc[dt][0]);
-          oacc[dt][1] = mfma16(a, pb[1][ks2], oacc[dt][1]);
+          oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, a8), pb[s], oacc[dt]);
         }
       }
     }
@@ -324,33 +329,35 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     stage ^= 1;
   }
 
-  // ---- epilogue ----
-#pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    float l = l_run[qt];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int qrow = r0w + 16 * qt + c;
-    if (qrow >= gm.Lq) continue;
+  // ---- epilogue: lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32] ----
+  float l = l_run + __shfl_xor(l_run, 32);
+  const int qrow = r0w + c32;
+  if (qrow < gm.Lq) {
     if (splits == 1) {
       const float inv = l > 0.f ? 1.0f / l : 0.f;
-      uint16_t* orow = o + ((size_t)bh * gm.Lq + qrow) * D + 4 * g;
+      uint16_t* orow = o + ((size_t)bh * gm.Lq + qrow) * D + 4 * h;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        u32x2 w;
-        w[0] = pack_bf16x2(oacc[dt][qt][0] * inv, oacc[dt][qt][1] * inv);
-        w[1] = pack_bf16x2(oacc[dt][qt][2] * inv, oacc[dt][qt][3] * inv);
-        *(u32x2*)(orow + 16 * dt) = w;
-      }
-      if (lse && g == 0)
-        lse[(size_t)bh * gm.Lq + qrow] = l > 0.f ? (m_run[qt] + log2f(l)) * 0.69314718055994531f : -INFINITY;
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          u32x2 w;
+          w[0] = pack_bf16x2(oacc[dt][4 * a4] * inv, oacc[dt][4 * a4 + 1] * inv);
+          w[1] = pack_bf16x2(oacc[dt][4 * a4 + 2] * inv, oacc[dt][4 * a4 + 3] * inv);
+          *(u32x2*)(orow + 32 * dt + 8 * a4) = w;
+        }
+      if (lse && h == 0)
+        lse[(size_t)bh * gm.Lq + qrow] = l > 0.f ? (m_run + log2f(l)) * 0.69314718055994531f : -INFINITY;
     } else {
       const size_t prow = ((size_t)sp * BH + bh) * gm.Lq + qrow;
-      float* po = part_o + prow * D + 4 * g;
+      float* po = part_o + prow * D + 4 * h;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) *(f32x4*)(po + 16 * dt) = oacc[dt][qt];
-      if (g == 0) {
-        part_m[prow] = m_run[qt];
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4)
+          *(f32x4*)(po + 32 * dt + 8 * a4) =
+              f32x4{oacc[dt][4 * a4], oacc[dt][4 * a4 + 1], oacc[dt][4 * a4 + 2], oacc[dt][4 * a4 + 3]};
+      if (h == 0) {
+        part_m[prow] = m_run;
         part_l[prow] = l;
       }
     }
