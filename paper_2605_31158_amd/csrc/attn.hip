@@ -8,10 +8,10 @@
 //     order (a two-pointer merge over the sorted lists).  Every kept block is staged once in
 //     LDS and consumed by the waves whose query block kept it; the other waves only help
 //     load.  Forced (chunk) blocks are kept by every query block, so most tiles are shared.
-//   * Key blocks are consumed in 64-key sub-tiles, staged by asynchronous buffer-to-LDS
+//   * Key blocks are consumed in 64-key sub-tiles staged by asynchronous buffer-to-LDS
 //     16-byte loads into a double buffer: sub-tile t+1 streams in while sub-tile t is
-//     multiplied, with one workgroup barrier per sub-tile.  The buffer descriptor of a
-//     sub-tile ends at Lk, so the ragged last block reads zeros past the end.
+//     multiplied, with one workgroup barrier per sub-tile.  The buffer descriptors end at Lk,
+//     so the ragged last block reads zeros past the end.
 //   * Workgroup ids are remapped so that each XCD (each L2) works on consecutive (head,
 //     row tile) units: the kept K/V blocks of a head stay hot in one XCD's L2.
 //   * Few work units (small problems) split the key-block range across workgroups; the
@@ -44,22 +44,24 @@ constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the running max 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 #define LDS_AS __attribute__((address_space(3)))
 
 __device__ inline f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  const f32x2v f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2v));
 }
 
-// LDS layout of one stage: a K tile and a V tile, each 64 key rows of D bf16, row-major with
-// padded rows.  K rows are padded to D*2 + 16 bytes: the 32 key rows an MFMA operand read
-// touches (16 per LDS cycle) start in distinct 16-byte bank groups.  V rows are padded to
-// D*2 + 64 bytes: a transpose read touches 4 rows x 64 contiguous bytes per half-wave, which
-// then cover all 64 banks exactly once.
+// LDS layout: K and V tiles of 64 key rows of D bf16, row-major with padded rows.  K rows are
+// padded to D*2 + 16 bytes: the 32 key rows an MFMA operand read touches (16 per LDS cycle)
+// start in distinct 16-byte bank groups.  V rows are padded to D*2 + 64 bytes: a transpose
+// read touches 4 rows x 64 contiguous bytes per half-wave, which then cover all 64 banks once.
 template <int D>
 struct Tile {
   static constexpr int KSTRIDE = D * 2 + 16;
@@ -72,7 +74,6 @@ struct Tile {
   static constexpr int VINST = KT * VSLOTS / 64;
   static constexpr int KPER = (KINST + 3) / 4;         // per wave (4 waves)
   static constexpr int VPER = (VINST + 3) / 4;
-  static constexpr int STAGE = KBYTES + VBYTES;
 };
 
 // Global byte offset (inside a tile of 64 rows) that lane `lane` of load `n` fetches so that it
@@ -85,34 +86,193 @@ __device__ inline uint32_t slot_offset(int n, int lane, int slots) {
   return chunk < D / 8 ? (uint32_t)(row * D * 2 + chunk * 16) : 0x7fffffffu;
 }
 
-// Issues this wave's buffer-to-LDS loads of one 64-key sub-tile (K and V) into `stage`.
-// The buffer descriptors start at the sub-tile and end at Lk, so rows past Lk (and the
-// padding slots, whose offsets lie past any buffer) read as zero.
-template <int D>
-__device__ inline void issue_tile(unsigned char* stage, const uint16_t* kh, const uint16_t* vh, int key0,
-                                  int Lk, const uint32_t* koff, const uint32_t* voff, int wave) {
-  using T = Tile<D>;
-  // a sub-tile may start at or past Lk (second half of a ragged 128-key block): no valid rows
+// Issues this wave's buffer-to-LDS loads of one 64-key tile of one matrix (NINST wave-wide
+// loads over the workgroup, PER per wave) into `dst`.  The descriptor starts at the tile and
+// ends at Lk: rows past Lk and padding slots read as zero.
+template <int D, int NINST, int PER>
+__device__ inline void issue_rows(unsigned char* dst, const uint16_t* base, int key0, int Lk, const uint32_t* off,
+                                  int wave) {
+  // a tile may start at or past Lk (second half of a ragged 128-key block): no valid rows
   const uint32_t nrec = key0 < Lk ? (uint32_t)(Lk - key0) * (uint32_t)(D * 2) : 0u;
-  const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc((void*)(kh + (size_t)key0 * D), 0, nrec, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc((void*)(vh + (size_t)key0 * D), 0, nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)key0 * D), 0, nrec, 0x00020000);
 #pragma unroll
-  for (int u = 0; u < T::KPER; ++u) {
+  for (int u = 0; u < PER; ++u) {
     const int n = wave + 4 * u;
-    if (T::KINST % 4 == 0 || n < T::KINST)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (LDS_AS void*)(stage + 1024 * n), 16, koff[u], 0, 0, 0);
-  }
-#pragma unroll
-  for (int u = 0; u < T::VPER; ++u) {
-    const int n = wave + 4 * u;
-    if (T::VINST % 4 == 0 || n < T::VINST)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (LDS_AS void*)(stage + T::KBYTES + 1024 * n), 16, voff[u], 0, 0, 0);
+    if (NINST % 4 == 0 || n < NINST)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void*)(dst + 1024 * n), 16, off[u], 0, 0, 0);
   }
 }
 
 struct Geom {
   int Lq, Lk, block, NQ, NK, F, chunk0;
 };
+
+// Per-wave constants of the tile loop.
+struct WaveCtx {
+  int key_lk;                // Lk
+  int klimit;                // keys >= klimit are invisible to this lane's query row
+  int klimit_wave;           // smallest klimit of the wave (tiles below it need no mask)
+  int kbase, vbase;          // LDS read bases of this lane inside a K / V tile
+  int h;                     // lane / 32
+  float scale_log2;
+};
+
+// S^T = K Q^T for one 64-key tile: two 32x32 accumulators (keys 0..31, 32..63).
+template <int D>
+__device__ __forceinline__ void qk_tile(const unsigned char* __restrict__ kb, const bf16x8* qreg, f32x16* sacc,
+                                        int kbase) {
+  using T = Tile<D>;
+  constexpr int KS = D / 16;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sacc[kt][i] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const bf16x8 a = *(const bf16x8*)(kb + kbase + kt * 32 * T::KSTRIDE + 32 * ks);
+      sacc[kt] = mfma32(a, qreg[ks], sacc[kt]);
+    }
+  }
+}
+
+// Masks (ragged tail, frame-causal pairs), running max and the lazy rescale of O for one tile.
+// Lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row.
+template <int D>
+__device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& m_run, float& l_run, int key0,
+                                             const WaveCtx& w) {
+  constexpr int DT = D / 32;
+  if (key0 + KT > w.klimit_wave) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = key0 + 32 * kt + 8 * (i >> 2) + 4 * w.h + (i & 3);
+        if (key >= w.klimit) sacc[kt][i] = -INFINITY;
+      }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float mt = mx * w.scale_log2;
+  const bool raise = mt > m_run + kRescaleSlack;
+  if (__any(raise)) {
+    const float m_new = raise ? mt : m_run;
+    const float alpha = raise ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+  }
+}
+
+// P = 2^(S*scale - m) (row sums in fp32, P rounded to bf16 for the product), then
+// O^T += V^T P^T with the V^T operand read by LDS transpose loads.
+template <int D>
+__device__ __forceinline__ void softmax_pv(const f32x16* sacc, const unsigned char* __restrict__ vb, f32x16* oacc,
+                                           float m_run, float& l_run, const WaveCtx& w) {
+  using T = Tile<D>;
+  constexpr int DT = D / 32;
+  const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+  float rs0 = 0.f, rs1 = 0.f;
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) {
+    u32x4 pw;
+#pragma unroll
+    for (int j2 = 0; j2 < 4; ++j2) {
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s4 >> 1][8 * (s4 & 1) + 2 * j2], w.scale_log2, -m_use));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s4 >> 1][8 * (s4 & 1) + 2 * j2 + 1], w.scale_log2, -m_use));
+      pw[j2] = pack_bf16x2(p0, p1);
+      rs0 += p0;
+      rs1 += p1;
+    }
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const unsigned char* va = vb + w.vbase + (16 * s4) * T::VSTRIDE + 64 * dt;
+      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va));
+      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va + 8 * T::VSTRIDE));
+      const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, a8), pb, oacc[dt]);
+    }
+  }
+  l_run += rs0 + rs1;
+}
+
+// A sub-tile of the merged walk: first key, and which of the two query blocks keep it.
+struct TileRef {
+  int key0;
+  bool a, b, valid;
+};
+
+// Walk over the merged kept lists of the workgroup's (up to) two query blocks.
+struct Walk {
+  const int32_t* la;
+  const int32_t* lb;
+  int na, nb, pa, pb, ja, jb, jhi;
+  int cj, csub, nsub, block;
+  bool cA, cB;
+  // next kept block of the merge, and which lists keep it; blocks at or past jhi end it
+  __device__ inline void pop() {
+    cj = min(ja, jb);
+    if (cj >= jhi) {
+      cj = kEnd;
+      cA = cB = false;
+      return;
+    }
+    cA = (ja == cj);
+    cB = (jb == cj);
+    if (cA) { ++pa; ja = pa < na ? la[pa] : kEnd; }
+    if (cB) { ++pb; jb = pb < nb ? lb[pb] : kEnd; }
+  }
+  __device__ inline TileRef next() {
+    TileRef t;
+    t.valid = cj != kEnd;
+    t.key0 = cj * block + csub * KT;
+    t.a = cA;
+    t.b = cB;
+    if (t.valid) {
+      if (++csub == nsub) {
+        csub = 0;
+        pop();
+      }
+    }
+    return t;
+  }
+};
+
+// One step of the double-buffered loop for sub-tile t, staged in (kcur, vcur); sub-tile t+1 is
+// issued into (knext, vnext) while t is multiplied.  The read and write buffers are distinct
+// __shared__ arrays, so the compiler can see that reads never wait on the asynchronous writes.
+template <int D>
+__device__ __forceinline__ void tile_step(const unsigned char* __restrict__ kcur, const unsigned char* __restrict__ vcur,
+                                          unsigned char* __restrict__ knext, unsigned char* __restrict__ vnext,
+                                          const TileRef& t0, const TileRef& t1, const uint16_t* kh,
+                                          const uint16_t* vh, const uint32_t* koff, const uint32_t* voff, int wave,
+                                          bool wave_b, bool wave_rows, const bf16x8* qreg, f32x16* oacc,
+                                          float& m_run, float& l_run, const WaveCtx& w) {
+  using T = Tile<D>;
+  // this thread's loads of (kcur, vcur) are done; the barrier makes every thread's loads
+  // visible and guarantees no wave still reads (knext, vnext), which held sub-tile t-1
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (t1.valid) {
+    issue_rows<D, T::KINST, T::KPER>(knext, kh, t1.key0, w.key_lk, koff, wave);
+    issue_rows<D, T::VINST, T::VPER>(vnext, vh, t1.key0, w.key_lk, voff, wave);
+  }
+  if ((wave_b ? t0.b : t0.a) && wave_rows) {
+    f32x16 sacc[2];
+    qk_tile<D>(kcur, qreg, sacc, w.kbase);
+    softmax_prep<D>(sacc, oacc, m_run, l_run, t0.key0, w);
+    softmax_pv<D>(sacc, vcur, oacc, m_run, l_run, w);
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
@@ -123,7 +283,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   using T = Tile<D>;
   constexpr int KS = D / 16;   // k-steps of Q.K^T (32x32x16)
   constexpr int DT = D / 32;   // d tiles of P.V
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * T::STAGE];
+  __shared__ __attribute__((aligned(1024))) unsigned char kbuf0[T::KBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char kbuf1[T::KBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char vbuf0[T::VBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char vbuf1[T::VBYTES];
 
   // XCD-aware id: hardware places consecutive workgroup ids on consecutive XCDs (round
   // robin over 8); give each XCD a contiguous range of logical units.
@@ -135,7 +298,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int rt = (logical / splits) % row_tiles;
   const int bh = logical / (splits * row_tiles);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps tile-issue math scalar
   const int c32 = lane & 31, h = lane >> 5;
   const int row_base = rt * QR;
   const int r0w = row_base + wave * QW;                 // first query row of this wave
@@ -145,21 +309,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const bool wave_b = two && wave >= 2;                 // waves 2, 3 own the second block
   const bool wave_rows = r0w < gm.Lq;
 
-  const int32_t* la_ = idx + ((size_t)bh * gm.NQ + qa) * gm.NK;
-  const int na = counts[(size_t)bh * gm.NQ + qa];
-  const int32_t* lb_ = qb >= 0 ? idx + ((size_t)bh * gm.NQ + qb) * gm.NK : la_;
-  const int nb = qb >= 0 ? counts[(size_t)bh * gm.NQ + qb] : 0;
-
+  Walk wk;
+  wk.la = idx + ((size_t)bh * gm.NQ + qa) * gm.NK;
+  wk.na = counts[(size_t)bh * gm.NQ + qa];
+  wk.lb = qb >= 0 ? idx + ((size_t)bh * gm.NQ + qb) * gm.NK : wk.la;
+  wk.nb = qb >= 0 ? counts[(size_t)bh * gm.NQ + qb] : 0;
   // split range of key blocks [jlo, jhi)
   const int jlo = (int)((int64_t)gm.NK * sp / splits);
-  const int jhi = (int)((int64_t)gm.NK * (sp + 1) / splits);
-  int pa = 0, pb = 0;
+  wk.jhi = (int)((int64_t)gm.NK * (sp + 1) / splits);
+  wk.pa = 0;
+  wk.pb = 0;
   if (splits > 1) {
-    while (pa < na && la_[pa] < jlo) ++pa;
-    while (pb < nb && lb_[pb] < jlo) ++pb;
+    while (wk.pa < wk.na && wk.la[wk.pa] < jlo) ++wk.pa;
+    while (wk.pb < wk.nb && wk.lb[wk.pb] < jlo) ++wk.pb;
   }
-  int ja = pa < na ? la_[pa] : kEnd;
-  int jb = pb < nb ? lb_[pb] : kEnd;
+  wk.ja = wk.pa < wk.na ? wk.la[wk.pa] : kEnd;
+  wk.jb = wk.pb < wk.nb ? wk.lb[wk.pb] : kEnd;
+  wk.nsub = gm.block / KT;
+  wk.block = gm.block;
+  wk.csub = 0;
+  wk.pop();
 
   const uint16_t* kh = k + (size_t)bh * gm.Lk * D;
   const uint16_t* vh = v + (size_t)bh * gm.Lk * D;
@@ -176,19 +345,35 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int n = wave + 4 * u;
     voff[u] = n < T::VINST ? slot_offset<D>(n, lane, T::VSLOTS) : 0x7fffffffu;
   }
+
   // Q^T operand (32x32x16 B): lane holds Q[row r0w + l%32][16 ks + 8 (l/32) .. + 7]
   bf16x8 qreg[KS];
   {
     const int row = r0w + c32;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      u32x4 w = u32x4{0u, 0u, 0u, 0u};
-      if (row < gm.Lq) w = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 16 * ks + 8 * h);
-      qreg[ks] = __builtin_bit_cast(bf16x8, w);
+      u32x4 qw = u32x4{0u, 0u, 0u, 0u};
+      if (row < gm.Lq) qw = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 16 * ks + 8 * h);
+      qreg[ks] = __builtin_bit_cast(bf16x8, qw);
     }
   }
-  const int qframe = gm.F > 0 ? (r0w + c32) / gm.F : 0;
-  const int wave_first_frame = gm.F > 0 ? r0w / gm.F : 0;
+  WaveCtx w;
+  w.key_lk = gm.Lk;
+  // Key n is visible to query row t when n < Lk and, with frames of F tokens inside the chunk,
+  // when its chunk frame is not later than t's: n < chunk0 + (t / F + 1) F (context keys,
+  // n < chunk0, always pass).  One limit per lane replaces the per-key frame arithmetic.
+  {
+    const int64_t lim = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)(r0w + c32) / gm.F + 1) * gm.F : (int64_t)gm.Lk;
+    const int64_t limw = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)r0w / gm.F + 1) * gm.F : (int64_t)gm.Lk;
+    w.klimit = (int)(lim < gm.Lk ? lim : gm.Lk);
+    w.klimit_wave = (int)(limw < gm.Lk ? limw : gm.Lk);
+  }
+  // LDS read bases: K operand row l%32, d offset 8 (l/32); V^T transpose read, 16-lane
+  // group G = l/16, lane i = l%16: row 4 (l/32) + i/4 of the 16-key step, d = 16 (G%2) + 4 (i%4).
+  w.kbase = c32 * T::KSTRIDE + 16 * h;
+  w.vbase = (4 * h + ((lane & 15) >> 2)) * T::VSTRIDE + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
+  w.h = h;
+  w.scale_log2 = scale_log2;
 
   f32x16 oacc[DT];
 #pragma unroll
@@ -198,136 +383,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   float m_run = -INFINITY;
   float l_run = 0.f;
 
-  // LDS read bases (bytes within a stage): K operand row l%32, d offset 8 (l/32);
-  // V^T transpose read, 16-lane group G = l/16, lane i = l%16: row 4 (l/32) + i/4 of the
-  // 16-key step, d = 16 (G%2) + 4 (i%4).
-  const int kbase = c32 * T::KSTRIDE + 16 * h;
-  const int vbase = T::KBYTES + (4 * h + ((lane & 15) >> 2)) * T::VSTRIDE + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
-
-  const int nsub = gm.block / KT;
-  // Merged walk over the two ascending lists: pop() yields the next kept block and which
-  // of the two query blocks keep it; blocks at or past jhi end the walk.
-  auto pop = [&](int& jj, bool& ua, bool& ub) {
-    jj = min(ja, jb);
-    if (jj >= jhi) {
-      jj = kEnd;
-      ua = ub = false;
-      return;
-    }
-    ua = (ja == jj);
-    ub = (jb == jj);
-    if (ua) { ++pa; ja = pa < na ? la_[pa] : kEnd; }
-    if (ub) { ++pb; jb = pb < nb ? lb_[pb] : kEnd; }
-  };
-  int cj, csub = 0;
-  bool cA, cB;
-  pop(cj, cA, cB);
-  int stage = 0;
-  if (cj != kEnd) issue_tile<D>(smem, kh, vh, cj * gm.block, gm.Lk, koff, voff, wave);
-  while (cj != kEnd) {
-    int nj = cj, nsb = csub + 1;
-    bool nA = cA, nB = cB;
-    if (nsb == nsub) {
-      nsb = 0;
-      pop(nj, nA, nB);
-    }
-    // this thread's loads of the current stage are done; the barrier makes every thread's
-    // loads visible and guarantees the other stage is no longer being read
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (nj != kEnd)
-      issue_tile<D>(smem + (stage ^ 1) * T::STAGE, kh, vh, nj * gm.block + nsb * KT, gm.Lk, koff, voff, wave);
-    const int key0 = cj * gm.block + csub * KT;
-    const bool mine = (wave_b ? cB : cA) && wave_rows;
-    const unsigned char* sb = smem + stage * T::STAGE;
-    if (mine) {
-      // ---- S^T = K Q^T : two 32x32 tiles over keys 0..31, 32..63 ----
-      f32x16 sacc[2];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sacc[kt][i] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          const bf16x8 a = *(const bf16x8*)(sb + kbase + kt * 32 * T::KSTRIDE + 32 * ks);
-          sacc[kt] = mfma32(a, qreg[ks], sacc[kt]);
-        }
-      }
-      // ---- masks: keys past Lk (ragged last block), frame-causal pairs in the chunk ----
-      // lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of query r0w + l%32
-      bool need_mask = key0 + KT > gm.Lk;
-      if (gm.F > 0 && key0 + KT - 1 >= gm.chunk0)
-        need_mask = need_mask || ((key0 + KT - 1 - gm.chunk0) / gm.F > wave_first_frame);
-      if (need_mask) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = key0 + 32 * kt + 8 * (i >> 2) + 4 * h + (i & 3);
-            bool ok = key < gm.Lk;
-            if (gm.F > 0 && key >= gm.chunk0) ok = ok && ((key - gm.chunk0) / gm.F <= qframe);
-            if (!ok) sacc[kt][i] = -INFINITY;
-          }
-      }
-      // ---- online softmax (base 2, scaled logits, lazy rescale) ----
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mt = mx * scale_log2;
-      const bool raise = mt > m_run + kRescaleSlack;
-      if (__any(raise)) {
-        const float m_new = raise ? mt : m_run;
-        const float alpha = raise ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
-      }
-      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-      float rs = 0.f;
-      bf16x8 pb[4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        float p[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          p[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s >> 1][8 * (s & 1) + j], scale_log2, -m_use));
-          rs += p[j];
-        }
-        u32x4 w;
-        w[0] = pack_bf16x2(p[0], p[1]);
-        w[1] = pack_bf16x2(p[2], p[3]);
-        w[2] = pack_bf16x2(p[4], p[5]);
-        w[3] = pack_bf16x2(p[6], p[7]);
-        pb[s] = __builtin_bit_cast(bf16x8, w);
-      }
-      l_run += rs;
-      // ---- O^T += V^T P^T : V^T operand by LDS transpose reads ----
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const unsigned char* va = sb + vbase + (16 * s) * T::VSTRIDE + 64 * dt;
-          const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va));
-          const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va + 8 * T::VSTRIDE));
-          const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, a8), pb[s], oacc[dt]);
-        }
-      }
-    }
-    cj = nj;
-    csub = nsb;
-    cA = nA;
-    cB = nB;
-    stage ^= 1;
+  TileRef t0 = wk.next(), t1 = wk.next();
+  if (t0.valid) {
+    issue_rows<D, T::KINST, T::KPER>(kbuf0, kh, t0.key0, gm.Lk, koff, wave);
+    issue_rows<D, T::VINST, T::VPER>(vbuf0, vh, t0.key0, gm.Lk, voff, wave);
   }
+  while (t0.valid) {
+    tile_step<D>(kbuf0, vbuf0, kbuf1, vbuf1, t0, t1, kh, vh, koff, voff, wave, wave_b, wave_rows, qreg, oacc,
+                 m_run, l_run, w);
+    t0 = t1;
+    t1 = wk.next();
+    if (!t0.valid) break;
+    tile_step<D>(kbuf1, vbuf1, kbuf0, vbuf0, t0, t1, kh, vh, koff, voff, wave, wave_b, wave_rows, qreg, oacc,
+                 m_run, l_run, w);
+    t0 = t1;
+    t1 = wk.next();
+  }
+  // no load is left in flight: the last step issued nothing (its t1 was invalid)
 
   // ---- epilogue: lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32] ----
   float l = l_run + __shfl_xor(l_run, 32);
@@ -340,10 +412,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4) {
-          u32x2 w;
-          w[0] = pack_bf16x2(oacc[dt][4 * a4] * inv, oacc[dt][4 * a4 + 1] * inv);
-          w[1] = pack_bf16x2(oacc[dt][4 * a4 + 2] * inv, oacc[dt][4 * a4 + 3] * inv);
-          *(u32x2*)(orow + 32 * dt + 8 * a4) = w;
+          u32x2 ow;
+          ow[0] = pack_bf16x2(oacc[dt][4 * a4] * inv, oacc[dt][4 * a4 + 1] * inv);
+          ow[1] = pack_bf16x2(oacc[dt][4 * a4 + 2] * inv, oacc[dt][4 * a4 + 3] * inv);
+          *(u32x2*)(orow + 32 * dt + 8 * a4) = ow;
         }
       if (lse && h == 0)
         lse[(size_t)bh * gm.Lq + qrow] = l > 0.f ? (m_run + log2f(l)) * 0.69314718055994531f : -INFINITY;
@@ -384,10 +456,10 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(const float* __r
   for (int e = 0; e < D / 64; ++e) acc[e] = 0.f;
   for (int s = 0; s < splits; ++s) {
     const size_t pr = (size_t)s * rows + wave;
-    const float w = exp2f(part_m[pr] - m_use);
-    l += w * part_l[pr];
+    const float wgt = exp2f(part_m[pr] - m_use);
+    l += wgt * part_l[pr];
 #pragma unroll
-    for (int e = 0; e < D / 64; ++e) acc[e] += w * part_o[pr * D + lane + 64 * e];
+    for (int e = 0; e < D / 64; ++e) acc[e] += wgt * part_o[pr * D + lane + 64 * e];
   }
   const float inv = l > 0.f ? 1.0f / l : 0.f;
 #pragma unroll
