@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps of the sparse path only (for rocprofv3), print the JSON anyway")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 256 MiB device-to-device copy (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -140,6 +142,13 @@ def main():
         la.sparse_attn_fwd(g["q"], g["k"], g["v"], cnt, ix, wl.block, n_text=wl.n_text, frame_tokens=F,
                            ws=ws, out=o)
 
+    if args.calibrate_copy:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         select()
         attn(counts, idx)
