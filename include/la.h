@@ -2,8 +2,7 @@
  * la.h -- C ABI of libla: block selection and block-sparse attention for
  * autoregressive (AR) chunk generation on AMD Instinct MI355X (gfx950).
  *
- * The operation is the "hardware-software co-designed 3D block sparse attention"
- * of Light Interaction (Sec. 3.3): a chunk of Lq query tokens (the frames being
+ * The operation is the block-sparse attention of Light Interaction (Sec. 3.3): a chunk of Lq query tokens (the frames being
  * denoised) attends to Lk keys laid out as
  *     [n_text text tokens][historical visual context][current chunk: last Lq keys].
  * Tokens are cut into 1-D blocks of `block` consecutive tokens.  Per (batch, head,
