@@ -1,5 +1,5 @@
 """Plain fp64 NumPy oracle for the AR block-sparse attention path of Light Interaction
-(Sec. 3.3, "Hardware-Software Co-designed 3D Sparse Attention").
+(Sec. 3.3).
 
 TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the bench's
 CPU-baseline leg, never by the GPU library.  Slow on purpose: every step is the
@@ -8,7 +8,7 @@ definition written out, one (batch, head, query block) at a time.
 Steps, in the paper's order and notation:
   * blocks: query blocks Q_i and key blocks K_m of `block` consecutive tokens
     (1-D blocks; the paper tiles 3-D (B_t, B_h, B_w) blocks, Sec. 3.3 and the
-    "Sparse attention configuration" paragraph of the appendix);
+    appendix's implementation details);
   * pooled proxies q_bar_i and k_bar_m: means over each block's tokens
     (Sec. 3.3, pooling equation);
   * relevance s_{i,m} = q_bar_i . k_bar_m / sqrt(d) over the M historical blocks
