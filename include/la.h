@@ -74,8 +74,9 @@ typedef struct la_shape {
 } la_shape;
 
 /* Bytes of scratch space la_select_blocks, la_select_blocks_topk and
- * la_sparse_attn_fwd need for this shape (the maximum over the three).
- * Returns 0 for an invalid shape. */
+ * la_sparse_attn_fwd need for this shape (the maximum over the three; the
+ * attention pass keeps its work plan and the partial results of work split
+ * across workgroups there).  Returns 0 for an invalid shape. */
 size_t la_workspace_bytes(const la_shape* shape);
 
 /* Cumulative-mass block selection.
@@ -104,9 +105,10 @@ la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void
 /* Block-sparse attention forward over the kept blocks.
  *   q bf16 [B, H, Lq, d]; k, v bf16 [B, H, Lk, d]                 (inputs)
  *   counts int32 [B, H, NQ], idx int32 [B, H, NQ, NK]: kept key blocks per query
- *          block, strictly ascending, each in [0, NK) (as written by
- *          la_select_blocks or la_mask_to_list; other lists are undefined
- *          behaviour).  One list serves both K and V (Sec. 3.3).
+ *          block in the first counts[] slots (as written by la_select_blocks or
+ *          la_mask_to_list).  The set of listed blocks is used: order and repeats
+ *          do not matter, entries outside [0, NK) are ignored and counts[] is
+ *          clamped to [0, NK].  One list serves both K and V (Sec. 3.3).
  *   scale  logit scale; <= 0 selects 1/sqrt(d).
  *   o      bf16 [B, H, Lq, d]: o_t = sum_n softmax_n(q_t . k_n * scale) v_n over
  *          the keys of the kept blocks visible to t; 0 when none is.

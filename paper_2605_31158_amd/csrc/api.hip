@@ -37,12 +37,6 @@ size_t select_ws_bytes(const Dims& dm) {
   return align256(qbar) + align256(scores);
 }
 
-size_t attn_ws_bytes(const Dims& dm, int splits) {
-  if (splits <= 1) return 0;
-  size_t rows = (size_t)splits * dm.BH * dm.Lq;
-  return align256(rows * dm.d * sizeof(float)) + 2 * align256(rows * sizeof(float));
-}
-
 }  // namespace la
 
 using namespace la;
@@ -55,7 +49,7 @@ size_t la_workspace_bytes(const la_shape* shape) {
   Dims dm;
   if (make_dims(shape, &dm) != LA_OK) return 0;
   size_t a = select_ws_bytes(dm);
-  size_t b = attn_ws_bytes(dm, attn_splits(dm));
+  size_t b = attn_ws_bytes(dm);
   return a > b ? a : b;
 }
 
@@ -96,10 +90,9 @@ la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k
   if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return LA_ERR_ARG;
   if (isnan(scale) || isinf(scale)) return LA_ERR_ARG;
   if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)dm.d);
-  int splits = attn_splits(dm);
-  size_t need = attn_ws_bytes(dm, splits);
-  if (need > 0 && (!ws || ws_bytes < need || ((uintptr_t)ws & 255u))) return LA_ERR_WORKSPACE;
-  hipError_t e = launch_attn(dm, q, k, v, counts, idx, scale, o, lse, ws, splits, (hipStream_t)stream);
+  size_t need = attn_ws_bytes(dm);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return LA_ERR_WORKSPACE;
+  hipError_t e = launch_attn(dm, q, k, v, counts, idx, scale, o, lse, ws, (hipStream_t)stream);
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 

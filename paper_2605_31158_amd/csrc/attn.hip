@@ -38,7 +38,6 @@ constexpr int kThreads = 256;
 constexpr int KT = 64;          // keys per sub-tile
 constexpr int QW = 32;          // query rows per wave
 constexpr int QR = 128;         // query rows per workgroup
-constexpr int kEnd = 0x7fffffff;
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the running max is raised
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -205,68 +204,140 @@ __device__ __forceinline__ void softmax_pv(const f32x16* sacc, const unsigned ch
   l_run += rs0 + rs1;
 }
 
-// A sub-tile of the merged walk: first key, and which of the two query blocks keep it.
+// ---------------------------------------------------------------------------
+// Work plan.  A unit is 128 consecutive query rows of one (batch, head): two query blocks of
+// 64 rows or one of 128 (list 0 = first block, list 1 = second).  Its tiles are the 64-key
+// sub-tiles of the union of its kept lists, in ascending block order; entry = block << 4 |
+// ownership bits (bit L: list L keeps the block).  A unit with no kept block still gets one
+// (unowned) tile so that some workgroup writes its output.
+
+constexpr int kPersist = 512;    // persistent workgroups: two per CU on a 256-CU MI355X
+
+__device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = x;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  __syncthreads();
+  if (lane == 63) sh[wave] = incl;
+  __syncthreads();
+  int base = 0, tot = 0;
+  for (int wv = 0; wv < (int)(blockDim.x >> 6); ++wv) {
+    if (wv < wave) base += sh[wv];
+    tot += sh[wv];
+  }
+  *total = tot;
+  return base + incl - x;
+}
+
+__global__ __launch_bounds__(kThreads) void plan_union_kernel(const int32_t* __restrict__ counts,
+                                                              const int32_t* __restrict__ idx, int NQ, int NK,
+                                                              int block, int row_tiles, int32_t* __restrict__ ulist,
+                                                              int32_t* __restrict__ ucount) {
+  extern __shared__ __align__(16) uint32_t own[];     // 4 ownership bits per key block
+  __shared__ int sh[kThreads / 64];
+  const int u = blockIdx.x;
+  const int bh = u / row_tiles, rt = u % row_tiles;
+  const int tid = threadIdx.x;
+  const int nwords = (NK + 7) >> 3;
+  for (int i = tid; i < nwords; i += kThreads) own[i] = 0;
+  __syncthreads();
+  const int q0 = rt * QR / block;
+  const int nlists = (block == 64 && q0 + 1 < NQ) ? 2 : 1;
+  for (int L = 0; L < nlists; ++L) {
+    const size_t row = (size_t)bh * NQ + q0 + L;
+    const int n = min(max(counts[row], 0), NK);
+    const int32_t* lst = idx + row * NK;
+    for (int i = tid; i < n; i += kThreads) {
+      const int j = lst[i];
+      if ((unsigned)j < (unsigned)NK) atomicOr(&own[j >> 3], (1u << L) << ((j & 7) * 4));
+    }
+  }
+  __syncthreads();
+  const int per = (nwords + kThreads - 1) / kThreads;
+  const int w0 = min(tid * per, nwords), w1 = min(w0 + per, nwords);
+  int cnt = 0;
+  for (int wi = w0; wi < w1; ++wi) {
+    const uint32_t x = own[wi];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cnt += ((x >> (4 * e)) & 15u) ? 1 : 0;
+  }
+  int total;
+  int pos = block_excl_scan_i(cnt, sh, &total);
+  int32_t* out = ulist + (size_t)u * NK;
+  for (int wi = w0; wi < w1; ++wi) {
+    const uint32_t x = own[wi];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t bits = (x >> (4 * e)) & 15u;
+      if (bits) out[pos++] = ((8 * wi + e) << 4) | (int)bits;
+    }
+  }
+  if (tid == 0) ucount[u] = total;
+}
+
+// tstart[u] = tiles of units < u (each unit max(1, blocks * nsub) tiles); tstart[U] = total.
+__global__ __launch_bounds__(1024) void plan_scan_kernel(const int32_t* __restrict__ ucount, int U, int nsub,
+                                                         int64_t* __restrict__ tstart) {
+  __shared__ int64_t sh[16];
+  __shared__ int64_t carry;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) carry = 0;
+  __syncthreads();
+  for (int base = 0; base < U; base += 1024) {
+    const int u = base + tid;
+    const int64_t x = u < U ? (int64_t)max(1, ucount[u] * nsub) : 0;
+    int64_t incl = x;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int64_t y = ((int64_t)__shfl_up((int)(incl >> 32), off) << 32) | (uint32_t)__shfl_up((int)incl, off);
+      if (lane >= off) incl += y;
+    }
+    if (lane == 63) sh[wave] = incl;
+    __syncthreads();
+    int64_t before = carry;
+    for (int wv = 0; wv < wave; ++wv) before += sh[wv];
+    if (u < U) tstart[u] = before + incl - x;
+    __syncthreads();
+    if (tid == 1023) carry = before + incl;
+    __syncthreads();
+  }
+  if (tid == 0) tstart[U] = carry;
+}
+
+// Persistent workgroup lambda covers tiles [T lambda / P, T (lambda + 1) / P) of the global
+// tile sequence.
+__device__ inline int64_t range_begin(int64_t T, int lambda, int P) { return T * lambda / P; }
+
+// One step of the double-buffered loop for tile i (staged in kcur, vcur); tile i+1 is issued
+// into (knext, vnext) while i is multiplied.  The read and write buffers are distinct
+// __shared__ arrays, so the compiler can see that reads never wait on the asynchronous writes.
 struct TileRef {
   int key0;
-  bool a, b, valid;
+  int bits;
+  bool valid;
 };
 
-// Walk over the merged kept lists of the workgroup's (up to) two query blocks.
-struct Walk {
-  const int32_t* la;
-  const int32_t* lb;
-  int na, nb, pa, pb, ja, jb, jhi;
-  int cj, csub, nsub, block;
-  bool cA, cB;
-  // next kept block of the merge, and which lists keep it; blocks at or past jhi end it
-  __device__ inline void pop() {
-    cj = min(ja, jb);
-    if (cj >= jhi) {
-      cj = kEnd;
-      cA = cB = false;
-      return;
-    }
-    cA = (ja == cj);
-    cB = (jb == cj);
-    if (cA) { ++pa; ja = pa < na ? la[pa] : kEnd; }
-    if (cB) { ++pb; jb = pb < nb ? lb[pb] : kEnd; }
-  }
-  __device__ inline TileRef next() {
-    TileRef t;
-    t.valid = cj != kEnd;
-    t.key0 = cj * block + csub * KT;
-    t.a = cA;
-    t.b = cB;
-    if (t.valid) {
-      if (++csub == nsub) {
-        csub = 0;
-        pop();
-      }
-    }
-    return t;
-  }
-};
-
-// One step of the double-buffered loop for sub-tile t, staged in (kcur, vcur); sub-tile t+1 is
-// issued into (knext, vnext) while t is multiplied.  The read and write buffers are distinct
-// __shared__ arrays, so the compiler can see that reads never wait on the asynchronous writes.
 template <int D>
 __device__ __forceinline__ void tile_step(const unsigned char* __restrict__ kcur, const unsigned char* __restrict__ vcur,
                                           unsigned char* __restrict__ knext, unsigned char* __restrict__ vnext,
                                           const TileRef& t0, const TileRef& t1, const uint16_t* kh,
                                           const uint16_t* vh, const uint32_t* koff, const uint32_t* voff, int wave,
-                                          bool wave_b, bool wave_rows, const bf16x8* qreg, f32x16* oacc,
+                                          int my_list, bool wave_rows, const bf16x8* qreg, f32x16* oacc,
                                           float& m_run, float& l_run, const WaveCtx& w) {
   using T = Tile<D>;
   // this thread's loads of (kcur, vcur) are done; the barrier makes every thread's loads
-  // visible and guarantees no wave still reads (knext, vnext), which held sub-tile t-1
+  // visible and guarantees no wave still reads (knext, vnext), which held tile i-1
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (t1.valid) {
     issue_rows<D, T::KINST, T::KPER>(knext, kh, t1.key0, w.key_lk, koff, wave);
     issue_rows<D, T::VINST, T::VPER>(vnext, vh, t1.key0, w.key_lk, voff, wave);
   }
-  if ((wave_b ? t0.b : t0.a) && wave_rows) {
+  if (((t0.bits >> my_list) & 1) && wave_rows) {
     f32x16 sacc[2];
     qk_tile<D>(kcur, qreg, sacc, w.kbase);
     softmax_prep<D>(sacc, oacc, m_run, l_run, t0.key0, w);
@@ -274,12 +345,26 @@ __device__ __forceinline__ void tile_step(const unsigned char* __restrict__ kcur
   }
 }
 
+__device__ inline TileRef tile_ref(const int32_t* __restrict__ ul, int64_t i, int64_t n, int nsub, int block,
+                                   int nblocks) {
+  TileRef t;
+  t.valid = i < n;
+  t.key0 = 0;
+  t.bits = 0;
+  if (t.valid && nblocks > 0) {
+    const int e = ul[nsub == 2 ? (i >> 1) : i];
+    t.key0 = (e >> 4) * block + (nsub == 2 ? (int)(i & 1) * KT : 0);
+    t.bits = e & 15;
+  }
+  return t;
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const int32_t* __restrict__ counts, const int32_t* __restrict__ idx, uint16_t* __restrict__ o,
-    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
-    float* __restrict__ part_l, Geom gm, int BH, int row_tiles, int splits, int units, float scale_log2) {
+    const int32_t* __restrict__ ulist, const int32_t* __restrict__ ucount, const int64_t* __restrict__ tstart,
+    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
+    float* __restrict__ part_l, Geom gm, int BH, int row_tiles, int U, float scale_log2) {
   using T = Tile<D>;
   constexpr int KS = D / 16;   // k-steps of Q.K^T (32x32x16)
   constexpr int DT = D / 32;   // d tiles of P.V
@@ -288,236 +373,286 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   __shared__ __attribute__((aligned(1024))) unsigned char vbuf0[T::VBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char vbuf1[T::VBYTES];
 
-  // XCD-aware id: hardware places consecutive workgroup ids on consecutive XCDs (round
-  // robin over 8); give each XCD a contiguous range of logical units.
-  const int per_xcd = gridDim.x >> 3;
-  const int hw = blockIdx.x;
-  const int logical = (hw & 7) * per_xcd + (hw >> 3);
-  if (logical >= units) return;
-  const int sp = logical % splits;
-  const int rt = (logical / splits) % row_tiles;
-  const int bh = logical / (splits * row_tiles);
+  // XCD-aware range: hardware places consecutive workgroup ids on consecutive XCDs (round
+  // robin over 8); the workgroups of one XCD get consecutive ranges, i.e. consecutive units
+  // of the same heads, so each L2 keeps its heads' shared K/V.
+  const int P = gridDim.x;
+  const int lambda = (blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3);
+  const int64_t Ttot = tstart[U];
+  const int64_t t_begin = range_begin(Ttot, lambda, P), t_end = range_begin(Ttot, lambda + 1, P);
+  if (t_begin >= t_end) return;
+  // unit holding t_begin: largest u with tstart[u] <= t_begin
+  int ulo = 0, uhi = U - 1;
+  while (ulo < uhi) {
+    const int mid = (ulo + uhi + 1) >> 1;
+    if (tstart[mid] <= t_begin) ulo = mid;
+    else uhi = mid - 1;
+  }
+  int u = ulo;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps tile-issue math scalar
   const int c32 = lane & 31, h = lane >> 5;
-  const int row_base = rt * QR;
-  const int r0w = row_base + wave * QW;                 // first query row of this wave
-  const bool two = (gm.block == 64);
-  const int qa = row_base / gm.block;
-  const int qb = (two && qa + 1 < gm.NQ) ? qa + 1 : -1;
-  const bool wave_b = two && wave >= 2;                 // waves 2, 3 own the second block
-  const bool wave_rows = r0w < gm.Lq;
-
-  Walk wk;
-  wk.la = idx + ((size_t)bh * gm.NQ + qa) * gm.NK;
-  wk.na = counts[(size_t)bh * gm.NQ + qa];
-  wk.lb = qb >= 0 ? idx + ((size_t)bh * gm.NQ + qb) * gm.NK : wk.la;
-  wk.nb = qb >= 0 ? counts[(size_t)bh * gm.NQ + qb] : 0;
-  // split range of key blocks [jlo, jhi)
-  const int jlo = (int)((int64_t)gm.NK * sp / splits);
-  wk.jhi = (int)((int64_t)gm.NK * (sp + 1) / splits);
-  wk.pa = 0;
-  wk.pb = 0;
-  if (splits > 1) {
-    while (wk.pa < wk.na && wk.la[wk.pa] < jlo) ++wk.pa;
-    while (wk.pb < wk.nb && wk.lb[wk.pb] < jlo) ++wk.pb;
-  }
-  wk.ja = wk.pa < wk.na ? wk.la[wk.pa] : kEnd;
-  wk.jb = wk.pb < wk.nb ? wk.lb[wk.pb] : kEnd;
-  wk.nsub = gm.block / KT;
-  wk.block = gm.block;
-  wk.csub = 0;
-  wk.pop();
-
-  const uint16_t* kh = k + (size_t)bh * gm.Lk * D;
-  const uint16_t* vh = v + (size_t)bh * gm.Lk * D;
+  const int nsub = gm.block / KT;
+  const int my_list = (gm.block == 64 && wave >= 2) ? 1 : 0;   // waves 2, 3 own the second block
 
   // lane-constant global offsets of this wave's tile loads
   uint32_t koff[T::KPER], voff[T::VPER];
 #pragma unroll
-  for (int u = 0; u < T::KPER; ++u) {
-    const int n = wave + 4 * u;
-    koff[u] = n < T::KINST ? slot_offset<D>(n, lane, T::KSLOTS) : 0x7fffffffu;
+  for (int uu = 0; uu < T::KPER; ++uu) {
+    const int n = wave + 4 * uu;
+    koff[uu] = n < T::KINST ? slot_offset<D>(n, lane, T::KSLOTS) : 0x7fffffffu;
   }
 #pragma unroll
-  for (int u = 0; u < T::VPER; ++u) {
-    const int n = wave + 4 * u;
-    voff[u] = n < T::VINST ? slot_offset<D>(n, lane, T::VSLOTS) : 0x7fffffffu;
-  }
-
-  // Q^T operand (32x32x16 B): lane holds Q[row r0w + l%32][16 ks + 8 (l/32) .. + 7]
-  bf16x8 qreg[KS];
-  {
-    const int row = r0w + c32;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      u32x4 qw = u32x4{0u, 0u, 0u, 0u};
-      if (row < gm.Lq) qw = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 16 * ks + 8 * h);
-      qreg[ks] = __builtin_bit_cast(bf16x8, qw);
-    }
+  for (int uu = 0; uu < T::VPER; ++uu) {
+    const int n = wave + 4 * uu;
+    voff[uu] = n < T::VINST ? slot_offset<D>(n, lane, T::VSLOTS) : 0x7fffffffu;
   }
   WaveCtx w;
   w.key_lk = gm.Lk;
-  // Key n is visible to query row t when n < Lk and, with frames of F tokens inside the chunk,
-  // when its chunk frame is not later than t's: n < chunk0 + (t / F + 1) F (context keys,
-  // n < chunk0, always pass).  One limit per lane replaces the per-key frame arithmetic.
-  {
-    const int64_t lim = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)(r0w + c32) / gm.F + 1) * gm.F : (int64_t)gm.Lk;
-    const int64_t limw = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)r0w / gm.F + 1) * gm.F : (int64_t)gm.Lk;
-    w.klimit = (int)(lim < gm.Lk ? lim : gm.Lk);
-    w.klimit_wave = (int)(limw < gm.Lk ? limw : gm.Lk);
-  }
-  // LDS read bases: K operand row l%32, d offset 8 (l/32); V^T transpose read, 16-lane
-  // group G = l/16, lane i = l%16: row 4 (l/32) + i/4 of the 16-key step, d = 16 (G%2) + 4 (i%4).
   w.kbase = c32 * T::KSTRIDE + 16 * h;
   w.vbase = (4 * h + ((lane & 15) >> 2)) * T::VSTRIDE + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
   w.h = h;
   w.scale_log2 = scale_log2;
 
-  f32x16 oacc[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
-  float m_run = -INFINITY;
-  float l_run = 0.f;
+  int64_t t = t_begin;
+  while (t < t_end) {
+    const int64_t ts = tstart[u], te = tstart[u + 1];
+    const int64_t a = t - ts, b = (te < t_end ? te : t_end) - ts;   // local tile range [a, b)
+    const bool full = (a == 0) && (b == te - ts);
+    const int bh = u / row_tiles, rt = u % row_tiles;
+    const int row_base = rt * QR;
+    const int r0w = row_base + wave * QW;               // first query row of this wave
+    const bool wave_rows = r0w < gm.Lq;
+    const int nblocks = ucount[u];
+    const int32_t* ul = ulist + (size_t)u * gm.NK;
+    const int64_t ntiles = (int64_t)nblocks * nsub;     // 0 for an empty unit (its dummy tile is unowned)
+    const uint16_t* kh = k + (size_t)bh * gm.Lk * D;
+    const uint16_t* vh = v + (size_t)bh * gm.Lk * D;
 
-  TileRef t0 = wk.next(), t1 = wk.next();
-  if (t0.valid) {
-    issue_rows<D, T::KINST, T::KPER>(kbuf0, kh, t0.key0, gm.Lk, koff, wave);
-    issue_rows<D, T::VINST, T::VPER>(vbuf0, vh, t0.key0, gm.Lk, voff, wave);
-  }
-  while (t0.valid) {
-    tile_step<D>(kbuf0, vbuf0, kbuf1, vbuf1, t0, t1, kh, vh, koff, voff, wave, wave_b, wave_rows, qreg, oacc,
-                 m_run, l_run, w);
-    t0 = t1;
-    t1 = wk.next();
-    if (!t0.valid) break;
-    tile_step<D>(kbuf1, vbuf1, kbuf0, vbuf0, t0, t1, kh, vh, koff, voff, wave, wave_b, wave_rows, qreg, oacc,
-                 m_run, l_run, w);
-    t0 = t1;
-    t1 = wk.next();
-  }
-  // no load is left in flight: the last step issued nothing (its t1 was invalid)
-
-  // ---- epilogue: lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32] ----
-  float l = l_run + __shfl_xor(l_run, 32);
-  const int qrow = r0w + c32;
-  if (qrow < gm.Lq) {
-    if (splits == 1) {
-      const float inv = l > 0.f ? 1.0f / l : 0.f;
-      uint16_t* orow = o + ((size_t)bh * gm.Lq + qrow) * D + 4 * h;
+    // Q^T operand (32x32x16 B): lane holds Q[row r0w + l%32][16 ks + 8 (l/32) .. + 7]
+    bf16x8 qreg[KS];
+    {
+      const int row = r0w + c32;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int a4 = 0; a4 < 4; ++a4) {
-          u32x2 ow;
-          ow[0] = pack_bf16x2(oacc[dt][4 * a4] * inv, oacc[dt][4 * a4 + 1] * inv);
-          ow[1] = pack_bf16x2(oacc[dt][4 * a4 + 2] * inv, oacc[dt][4 * a4 + 3] * inv);
-          *(u32x2*)(orow + 32 * dt + 8 * a4) = ow;
-        }
-      if (lse && h == 0)
-        lse[(size_t)bh * gm.Lq + qrow] = l > 0.f ? (m_run + log2f(l)) * 0.69314718055994531f : -INFINITY;
-    } else {
-      const size_t prow = ((size_t)sp * BH + bh) * gm.Lq + qrow;
-      float* po = part_o + prow * D + 4 * h;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int a4 = 0; a4 < 4; ++a4)
-          *(f32x4*)(po + 32 * dt + 8 * a4) =
-              f32x4{oacc[dt][4 * a4], oacc[dt][4 * a4 + 1], oacc[dt][4 * a4 + 2], oacc[dt][4 * a4 + 3]};
-      if (h == 0) {
-        part_m[prow] = m_run;
-        part_l[prow] = l;
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 qw = u32x4{0u, 0u, 0u, 0u};
+        if (row < gm.Lq) qw = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 16 * ks + 8 * h);
+        qreg[ks] = __builtin_bit_cast(bf16x8, qw);
       }
+    }
+    // Key n is visible to query row t when n < Lk and, with frames of F tokens inside the chunk,
+    // when its chunk frame is not later than t's: n < chunk0 + (t / F + 1) F (context keys,
+    // n < chunk0, always pass).  One limit per lane replaces per-key frame arithmetic.
+    {
+      const int64_t lim = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)(r0w + c32) / gm.F + 1) * gm.F : (int64_t)gm.Lk;
+      const int64_t limw = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)r0w / gm.F + 1) * gm.F : (int64_t)gm.Lk;
+      w.klimit = (int)(lim < gm.Lk ? lim : gm.Lk);
+      w.klimit_wave = (int)(limw < gm.Lk ? limw : gm.Lk);
+    }
+    f32x16 oacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+
+    const int64_t bb = b < ntiles ? b : ntiles;         // real tiles of this piece (dummy tile: none)
+    // previous unit's last tile may still be read from either buffer: sync before refilling
+    __syncthreads();
+    TileRef t0 = tile_ref(ul, a, bb, nsub, gm.block, nblocks);
+    TileRef t1 = tile_ref(ul, a + 1, bb, nsub, gm.block, nblocks);
+    if (t0.valid) {
+      issue_rows<D, T::KINST, T::KPER>(kbuf0, kh, t0.key0, gm.Lk, koff, wave);
+      issue_rows<D, T::VINST, T::VPER>(vbuf0, vh, t0.key0, gm.Lk, voff, wave);
+    }
+    int64_t i = a;
+    while (t0.valid) {
+      tile_step<D>(kbuf0, vbuf0, kbuf1, vbuf1, t0, t1, kh, vh, koff, voff, wave, my_list, wave_rows, qreg, oacc,
+                   m_run, l_run, w);
+      ++i;
+      t0 = t1;
+      t1 = tile_ref(ul, i + 1, bb, nsub, gm.block, nblocks);
+      if (!t0.valid) break;
+      tile_step<D>(kbuf1, vbuf1, kbuf0, vbuf0, t0, t1, kh, vh, koff, voff, wave, my_list, wave_rows, qreg, oacc,
+                   m_run, l_run, w);
+      ++i;
+      t0 = t1;
+      t1 = tile_ref(ul, i + 1, bb, nsub, gm.block, nblocks);
+    }
+    // no load is left in flight: the last step issued nothing (its next tile was invalid)
+
+    // ---- output: lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32] ----
+    const float l = l_run + __shfl_xor(l_run, 32);
+    const int qrow = r0w + c32;
+    if (qrow < gm.Lq) {
+      if (full) {
+        const float inv = l > 0.f ? 1.0f / l : 0.f;
+        uint16_t* orow = o + ((size_t)bh * gm.Lq + qrow) * D + 4 * h;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int a4 = 0; a4 < 4; ++a4) {
+            u32x2 ow;
+            ow[0] = pack_bf16x2(oacc[dt][4 * a4] * inv, oacc[dt][4 * a4 + 1] * inv);
+            ow[1] = pack_bf16x2(oacc[dt][4 * a4 + 2] * inv, oacc[dt][4 * a4 + 3] * inv);
+            *(u32x2*)(orow + 32 * dt + 8 * a4) = ow;
+          }
+        if (lse && h == 0)
+          lse[(size_t)bh * gm.Lq + qrow] = l > 0.f ? (m_run + log2f(l)) * 0.69314718055994531f : -INFINITY;
+      } else {
+        // a piece of a unit split across workgroups: the workgroup's first unit goes to slot
+        // 2 lambda, its last (when it continues past the range) to slot 2 lambda + 1
+        const int slot = 2 * lambda + (a > 0 ? 0 : 1);
+        const size_t prow = (size_t)slot * QR + (qrow - row_base);
+        float* po = part_o + prow * D + 4 * h;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int a4 = 0; a4 < 4; ++a4)
+            *(f32x4*)(po + 32 * dt + 8 * a4) =
+                f32x4{oacc[dt][4 * a4], oacc[dt][4 * a4 + 1], oacc[dt][4 * a4 + 2], oacc[dt][4 * a4 + 3]};
+        if (h == 0) {
+          part_m[prow] = m_run;
+          part_l[prow] = l;
+        }
+      }
+    }
+    t = ts + b;
+    ++u;
+  }
+}
+
+// Merges the pieces of units that were split across workgroups:
+// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s, over the pieces in workgroup order
+// (deterministic).  Thread t owns 4 columns and QR * D / (4 * kThreads) rows of the unit, so
+// the loads of all its rows are in flight together.
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_combine_kernel(const int64_t* __restrict__ tstart, int U, int P,
+                                                                int row_tiles, int Lq,
+                                                                const float* __restrict__ part_o,
+                                                                const float* __restrict__ part_m,
+                                                                const float* __restrict__ part_l,
+                                                                uint16_t* __restrict__ o, float* __restrict__ lse) {
+  constexpr int CG = D / 4;                 // 4-column groups per row
+  constexpr int RSTEP = kThreads / CG;      // rows per pass
+  constexpr int NI = QR / RSTEP;            // rows per thread
+  const int u = blockIdx.x;
+  const int64_t Ttot = tstart[U], ts = tstart[u], te = tstart[u + 1];
+  // workgroup (range) holding tile t: largest lambda with T lambda / P <= t
+  auto owner = [&](int64_t t) {
+    int64_t lam = ((t + 1) * P + Ttot - 1) / Ttot - 1;
+    return (int)(lam < P - 1 ? lam : P - 1);
+  };
+  const int la0 = owner(ts), la1 = owner(te - 1);
+  if (la0 == la1) return;                               // not split: written directly
+  const int bh = u / row_tiles, rt = u % row_tiles;
+  const int cg = threadIdx.x % CG, r0 = threadIdx.x / CG;
+  float m[NI], l[NI];
+  f32x4 acc[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    m[i] = -INFINITY;
+    l[i] = 0.f;
+    acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // workgroups with an empty range (fewer tiles than workgroups) wrote no slot
+  for (int lam = la0; lam <= la1; ++lam) {
+    if (range_begin(Ttot, lam, P) == range_begin(Ttot, lam + 1, P)) continue;
+    const int slot = lam == la0 ? 2 * lam + 1 : 2 * lam;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) m[i] = fmaxf(m[i], part_m[(size_t)slot * QR + r0 + RSTEP * i]);
+  }
+  for (int lam = la0; lam <= la1; ++lam) {
+    if (range_begin(Ttot, lam, P) == range_begin(Ttot, lam + 1, P)) continue;
+    const int slot = lam == la0 ? 2 * lam + 1 : 2 * lam;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const size_t pr = (size_t)slot * QR + r0 + RSTEP * i;
+      const float wgt = exp2f(part_m[pr] - (m[i] == -INFINITY ? 0.f : m[i]));
+      l[i] += wgt * part_l[pr];
+      const f32x4 po = *(const f32x4*)(part_o + pr * D + 4 * cg);
+      acc[i] += wgt * po;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int qrow = rt * QR + r0 + RSTEP * i;
+    if (qrow < Lq) {
+      const float inv = l[i] > 0.f ? 1.0f / l[i] : 0.f;
+      u32x2 ow;
+      ow[0] = pack_bf16x2(acc[i][0] * inv, acc[i][1] * inv);
+      ow[1] = pack_bf16x2(acc[i][2] * inv, acc[i][3] * inv);
+      *(u32x2*)(o + ((size_t)bh * Lq + qrow) * D + 4 * cg) = ow;
+      if (lse && cg == 0)
+        lse[(size_t)bh * Lq + qrow] = l[i] > 0.f ? (m[i] + log2f(l[i])) * 0.69314718055994531f : -INFINITY;
     }
   }
 }
 
-// Merges split partials: O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s.
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_combine_kernel(const float* __restrict__ part_o,
-                                                                const float* __restrict__ part_m,
-                                                                const float* __restrict__ part_l,
-                                                                uint16_t* __restrict__ o, float* __restrict__ lse,
-                                                                int rows, int splits) {
-  // one wave per query row, lanes over d
-  const int wave = (blockIdx.x * kThreads + threadIdx.x) >> 6;
-  const int lane = threadIdx.x & 63;
-  if (wave >= rows) return;
-  float m = -INFINITY;
-  for (int s = 0; s < splits; ++s) m = fmaxf(m, part_m[(size_t)s * rows + wave]);
-  const float m_use = (m == -INFINITY) ? 0.f : m;
-  float l = 0.f;
-  float acc[D / 64];
-#pragma unroll
-  for (int e = 0; e < D / 64; ++e) acc[e] = 0.f;
-  for (int s = 0; s < splits; ++s) {
-    const size_t pr = (size_t)s * rows + wave;
-    const float wgt = exp2f(part_m[pr] - m_use);
-    l += wgt * part_l[pr];
-#pragma unroll
-    for (int e = 0; e < D / 64; ++e) acc[e] += wgt * part_o[pr * D + lane + 64 * e];
-  }
-  const float inv = l > 0.f ? 1.0f / l : 0.f;
-#pragma unroll
-  for (int e = 0; e < D / 64; ++e) {
-    const __bf16 b = (__bf16)(acc[e] * inv);
-    o[(size_t)wave * D + lane + 64 * e] = __builtin_bit_cast(uint16_t, b);
-  }
-  if (lse && lane == 0) lse[wave] = l > 0.f ? (m + log2f(l)) * 0.69314718055994531f : -INFINITY;
+struct AttnWs {
+  int32_t* ulist;
+  int32_t* ucount;
+  int64_t* tstart;
+  float* part_o;
+  float* part_m;
+  float* part_l;
+  size_t bytes;
+};
+
+AttnWs attn_ws_layout(const Dims& dm, void* base) {
+  const int row_tiles = ceil_div(dm.Lq, QR);
+  const size_t U = (size_t)dm.BH * row_tiles;
+  const size_t slots = 2 * (size_t)kPersist;
+  size_t off = 0;
+  AttnWs w;
+  char* b = (char*)base;
+  w.ulist = (int32_t*)(b + off);
+  off += align256(U * dm.NK * sizeof(int32_t));
+  w.ucount = (int32_t*)(b + off);
+  off += align256(U * sizeof(int32_t));
+  w.tstart = (int64_t*)(b + off);
+  off += align256((U + 1) * sizeof(int64_t));
+  w.part_o = (float*)(b + off);
+  off += align256(slots * QR * dm.d * sizeof(float));
+  w.part_m = (float*)(b + off);
+  off += align256(slots * QR * sizeof(float));
+  w.part_l = (float*)(b + off);
+  off += align256(slots * QR * sizeof(float));
+  w.bytes = off;
+  return w;
 }
 
 }  // namespace
 
-int attn_splits(const Dims& dm) {
-  const int row_tiles = ceil_div(dm.Lq, QR);
-  const int units = dm.BH * row_tiles;
-  const int target = 512;      // two workgroups per CU on a 256-CU MI355X
-  if (units >= target / 2) return 1;
-  int s = ceil_div(target, units);
-  s = s > 16 ? 16 : s;
-  s = s > dm.NK ? dm.NK : s;
-  return s < 1 ? 1 : s;
-}
+size_t attn_ws_bytes(const Dims& dm) { return attn_ws_layout(dm, nullptr).bytes; }
 
 hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void* v, const int32_t* counts,
-                       const int32_t* idx, float scale, void* o, float* lse, void* ws, int splits,
-                       hipStream_t st) {
+                       const int32_t* idx, float scale, void* o, float* lse, void* ws, hipStream_t st) {
   const int row_tiles = ceil_div(dm.Lq, QR);
-  const int units = dm.BH * row_tiles * splits;
-  const int grid = ceil_div(units, 8) * 8;
+  const int U = dm.BH * row_tiles;
+  const int nsub = dm.block / KT;
+  AttnWs w = attn_ws_layout(dm, ws);
   Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
   const float scale_log2 = scale * 1.4426950408889634f;
-  float* part_o = nullptr;
-  float* part_m = nullptr;
-  float* part_l = nullptr;
-  if (splits > 1) {
-    const size_t rows = (size_t)splits * dm.BH * dm.Lq;
-    part_o = (float*)ws;
-    part_m = (float*)((char*)ws + align256(rows * dm.d * sizeof(float)));
-    part_l = (float*)((char*)part_m + align256(rows * sizeof(float)));
-  }
+  hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t), st,
+                     counts, idx, dm.NQ, dm.NK, dm.block, row_tiles, w.ulist, w.ucount);
+  hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(1024), 0, st, w.ucount, U, nsub, w.tstart);
   if (dm.d == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(grid), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, counts, idx, (uint16_t*)o, lse, part_o, part_m,
-                       part_l, gm, dm.BH, row_tiles, splits, units, scale_log2);
+    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(kPersist), dim3(kThreads), 0, st, (const uint16_t*)q,
+                       (const uint16_t*)k, (const uint16_t*)v, w.ulist, w.ucount, w.tstart, (uint16_t*)o, lse,
+                       w.part_o, w.part_m, w.part_l, gm, dm.BH, row_tiles, U, scale_log2);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(grid), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, counts, idx, (uint16_t*)o, lse, part_o, part_m,
-                       part_l, gm, dm.BH, row_tiles, splits, units, scale_log2);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits == 1) return e;
-  const int rows = dm.BH * dm.Lq;
-  const int cgrid = ceil_div(rows * 64, kThreads);
+    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(kPersist), dim3(kThreads), 0, st, (const uint16_t*)q,
+                       (const uint16_t*)k, (const uint16_t*)v, w.ulist, w.ucount, w.tstart, (uint16_t*)o, lse,
+                       w.part_o, w.part_m, w.part_l, gm, dm.BH, row_tiles, U, scale_log2);
   if (dm.d == 128)
-    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(cgrid), dim3(kThreads), 0, st, part_o, part_m, part_l,
-                       (uint16_t*)o, lse, rows, splits);
+    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(U), dim3(kThreads), 0, st, w.tstart, U, kPersist, row_tiles,
+                       dm.Lq, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(cgrid), dim3(kThreads), 0, st, part_o, part_m, part_l,
-                       (uint16_t*)o, lse, rows, splits);
+    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(U), dim3(kThreads), 0, st, w.tstart, U, kPersist, row_tiles,
+                       dm.Lq, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   return hipGetLastError();
 }
 

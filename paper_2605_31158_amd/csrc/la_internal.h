@@ -32,10 +32,9 @@ la_status make_dims(const la_shape* s, Dims* out);
 
 // Workspace layout of the selection pass: pooled queries then the score matrix.
 size_t select_ws_bytes(const Dims& dm);
-// Workspace of the attention pass for a given split count (partials + row stats).
-size_t attn_ws_bytes(const Dims& dm, int splits);
-// Split factor the attention pass uses for this shape (1 = no split).
-int attn_splits(const Dims& dm);
+// Workspace of the attention pass: work plan (union lists, tile prefix sums) and the partial
+// (O, m, l) slots of units split across persistent workgroups.
+size_t attn_ws_bytes(const Dims& dm);
 
 // Launchers (defined next to their kernels); they only enqueue.
 hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau, int keep_fixed,
@@ -44,7 +43,7 @@ hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* cou
                                hipStream_t st);
 hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void* v,
                        const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
-                       void* ws, int splits, hipStream_t st);
+                       void* ws, hipStream_t st);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

@@ -74,6 +74,36 @@ def test_attn_empty_rows_and_custom_scale():
     assert (o[0, 0, :64] == 0).all() and np.isneginf(lse[0, 0, :64]).all()
 
 
+def test_attn_list_is_a_set():
+    # the attention pass uses the set of listed blocks: shuffled order, repeats, entries
+    # outside [0, NK) and counts beyond NK must give the same result as the clean list
+    B, H, Lq, Lk, d, block = 1, 3, 300, 1300, 128, 64
+    inp = make_clustered(B, H, Lq, Lk, d, block, 11)
+    rng = np.random.default_rng(11)
+    NQ, NK = -(-Lq // block), -(-Lk // block)
+    mask = (rng.uniform(size=(B, H, NQ, NK)) < 0.45).astype(np.uint8)
+    counts = np.zeros((B, H, NQ), np.int32)
+    idx = np.full((B, H, NQ, NK), -7, np.int32)
+    for h in range(H):
+        for i in range(NQ):
+            kept = np.nonzero(mask[0, h, i])[0]
+            junk = [NK, NK + 5, -1]
+            lst = list(kept) + list(rng.choice(kept, size=min(3, len(kept)))) + junk if len(kept) else junk
+            lst = list(rng.permutation(lst))[:NK]
+            counts[0, h, i] = len(lst)
+            idx[0, h, i, :len(lst)] = lst
+    counts[0, 1, 0] = NK + 100          # beyond NK: clamped, the rest of the row is -7 (ignored)
+    idx[0, 1, 0, :] = -7
+    kept = np.nonzero(mask[0, 1, 0])[0]
+    idx[0, 1, 0, :len(kept)] = kept[::-1]
+    g = to_gpu(inp)
+    o, lse = la.sparse_attn_fwd(g["q"], g["k"], g["v"], torch.from_numpy(counts).cuda(),
+                                torch.from_numpy(idx).cuda(), block, want_lse=True)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = O.attention(inp["q"], inp["k"], inp["v"], mask, block)
+    compare(bf16_tensor_to_f64(o), lse.cpu().numpy().astype(np.float64), o_ref, lse_ref, "list as a set")
+
+
 def test_attn_value_invariants():
     # V = 1 gives O = 1 exactly representable; one-hot V gives rows of weights summing to 1
     inp = make_clustered(1, 1, 128, 512, 64, 64, 8, v_kind="ones")
