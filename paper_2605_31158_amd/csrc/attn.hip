@@ -2,22 +2,34 @@
 // one kept-block list per query block serving both K and V).
 //
 // Work decomposition
-//   * A workgroup (4 waves) owns 128 consecutive query rows of one (batch, head): two query
-//     blocks of 64 rows, or one of 128.  Each wave owns 32 rows, all inside one query block.
-//   * The workgroup walks the union of its query blocks' kept lists in ascending block
-//     order (a two-pointer merge over the sorted lists).  Every kept block is staged once in
-//     LDS and consumed by the waves whose query block kept it; the other waves only help
-//     load.  Forced (chunk) blocks are kept by every query block, so most tiles are shared.
-//   * Key blocks are consumed in 64-key sub-tiles staged by asynchronous buffer-to-LDS
-//     16-byte loads into a double buffer: sub-tile t+1 streams in while sub-tile t is
-//     multiplied, with one workgroup barrier per sub-tile.  The buffer descriptors end at Lk,
-//     so the ragged last block reads zeros past the end.
-//   * Workgroup ids are remapped so that each XCD (each L2) works on consecutive (head,
-//     row tile) units: the kept K/V blocks of a head stay hot in one XCD's L2.
-//   * Few work units (small problems) split the key-block range across workgroups; the
-//     partial (O, m, l) are merged by attn_combine (log-sum-exp merge).
+//   * A unit is 256 consecutive query rows of one (batch, head): four query blocks of 64 rows
+//     or two of 128.  Its tiles are the 64-key sub-tiles of the union of its blocks' kept
+//     lists, in ascending key order, each tagged with which of the unit's blocks kept it.
+//   * A planner (three small kernels) builds every unit's union list, the prefix sum of the
+//     units' tile counts and one record per tile (first key, head, row tile, ownership).
+//     One persistent workgroup per CU then takes an equal share of the concatenated tile
+//     sequence (stream-K); a unit cut between two workgroups leaves
+//     (O, m, l) partials that attn_combine merges with a log-sum-exp merge.  Heavy query
+//     blocks therefore never bound the launch.
+//   * Workgroup ranges are laid out so that the workgroups of one XCD hold consecutive units,
+//     i.e. the same heads: the shared chunk K/V of a head stays in that XCD's L2.
 //
-// Per wave and 64-key sub-tile (d = 128):
+// The workgroup: 8 waves = two groups of four, one wave of each group per SIMD.  Each wave owns
+// 32 query rows; the two waves of a SIMD own the two halves of the same query block, so both
+// groups own the same tiles.  The groups run a ping-pong over the tile sequence, offset by one
+// phase and separated by workgroup barriers:
+//
+//   phase    group 0                          group 1
+//   A(h)     M(h): P.V of tile h-1, Q.K^T h   V(h-1): softmax of tile h-1; load K(h+1), V(h)
+//   B(h)     V(h): softmax of tile h          M(h): P.V of tile h-1, Q.K^T of tile h
+//
+// so on every SIMD one wave feeds the matrix pipeline while the other does the softmax
+// arithmetic.  K and V tiles live in two-stage LDS rings each (K(h) is read in A(h) and B(h),
+// V(h) in A(h+1) and B(h+1)); group 1 issues the asynchronous buffer-to-LDS loads of K(h+1) and
+// V(h) in A(h) and waits for them at the end of B(h).  The loads' buffer descriptors end at Lk,
+// so the ragged last block reads zeros past the end.
+//
+// Per wave and 64-key tile (d = 128):
 //   S^T (64 keys x 32 queries) = K_tile (64 x d) . Q^T       16 x v_mfma_f32_32x32x16_bf16
 //   online softmax over keys (fp32, base 2; the running max is only raised when a tile's
 //   max exceeds it by more than 2^8, so most tiles skip the rescale of O)
@@ -29,16 +41,22 @@
 // ds_read_b64_tr_b16 (two per MFMA).
 #include <math.h>
 
+#include <type_traits>
+
 #include "la_internal.h"
 
 namespace la {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int KT = 64;          // keys per sub-tile
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int KT = 64;          // keys per tile
 constexpr int QW = 32;          // query rows per wave
-constexpr int QR = 128;         // query rows per workgroup
+constexpr int QR = 256;         // query rows per unit (workgroup)
+constexpr int kMaxPersist = 256;        // persistent workgroups: one per CU, at most 256
 constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the running max is raised
+// flags of a tile record (see TileRef)
+constexpr int kFlFrom0 = 1 << 4, kFlToEnd = 1 << 5, kFlFirst = 1 << 6, kFlLast = 1 << 7, kFlValid = 1 << 8;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
@@ -57,6 +75,24 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2v));
 }
 
+// Workgroup barrier that orders LDS accesses only: the asynchronous tile loads in flight
+// (tracked by vmcnt) are not waited for.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Workgroup barrier for a wave with asynchronous tile loads in flight that it does not wait for
+// here: the LDS release fence of lds_barrier would wait for them (they write LDS).  The empty
+// asm statements keep the compiler from moving memory accesses across the barrier; the wave
+// has no LDS access of its own outstanding at this point.
+__device__ __forceinline__ void barrier_keep_loads() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // LDS layout: K and V tiles of 64 key rows of D bf16, row-major with padded rows.  K rows are
 // padded to D*2 + 16 bytes: the 32 key rows an MFMA operand read touches (16 per LDS cycle)
 // start in distinct 16-byte bank groups.  V rows are padded to D*2 + 64 bytes: a transpose
@@ -71,7 +107,7 @@ struct Tile {
   static constexpr int VBYTES = KT * VSTRIDE;
   static constexpr int KINST = KT * KSLOTS / 64;       // wave-wide 1 KiB loads per K tile
   static constexpr int VINST = KT * VSLOTS / 64;
-  static constexpr int KPER = (KINST + 3) / 4;         // per wave (4 waves)
+  static constexpr int KPER = (KINST + 3) / 4;         // per loading wave (4 waves load)
   static constexpr int VPER = (VINST + 3) / 4;
 };
 
@@ -85,18 +121,18 @@ __device__ inline uint32_t slot_offset(int n, int lane, int slots) {
   return chunk < D / 8 ? (uint32_t)(row * D * 2 + chunk * 16) : 0x7fffffffu;
 }
 
-// Issues this wave's buffer-to-LDS loads of one 64-key tile of one matrix (NINST wave-wide
-// loads over the workgroup, PER per wave) into `dst`.  The descriptor starts at the tile and
-// ends at Lk: rows past Lk and padding slots read as zero.
+// Issues this wave's share (loading wave lw of 4) of the buffer-to-LDS loads of one 64-key
+// tile of one matrix into `dst`.  The descriptor starts at the tile and ends at Lk: rows past
+// Lk and padding slots read as zero.
 template <int D, int NINST, int PER>
 __device__ inline void issue_rows(unsigned char* dst, const uint16_t* base, int key0, int Lk, const uint32_t* off,
-                                  int wave) {
+                                  int lw) {
   // a tile may start at or past Lk (second half of a ragged 128-key block): no valid rows
   const uint32_t nrec = key0 < Lk ? (uint32_t)(Lk - key0) * (uint32_t)(D * 2) : 0u;
   const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)key0 * D), 0, nrec, 0x00020000);
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
-    const int n = wave + 4 * u;
+    const int n = lw + 4 * u;
     if (NINST % 4 == 0 || n < NINST)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void*)(dst + 1024 * n), 16, off[u], 0, 0, 0);
   }
@@ -106,7 +142,7 @@ struct Geom {
   int Lq, Lk, block, NQ, NK, F, chunk0;
 };
 
-// Per-wave constants of the tile loop.
+// Per-wave constants of the tile loop (klimit, klimit_wave change with the unit).
 struct WaveCtx {
   int key_lk;                // Lk
   int klimit;                // keys >= klimit are invisible to this lane's query row
@@ -116,28 +152,69 @@ struct WaveCtx {
   float scale_log2;
 };
 
-// S^T = K Q^T for one 64-key tile: two 32x32 accumulators (keys 0..31, 32..63).
+// Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSgMfma = 0x008;
+constexpr int kSgDsRead = 0x100;
+
+// S^T = K Q^T for one 64-key tile: two 32x32 accumulators (keys 0..31, 32..63).  The K operand
+// reads run four MFMAs ahead of their use, so LDS latency overlaps the matrix pipeline.
 template <int D>
 __device__ __forceinline__ void qk_tile(const unsigned char* __restrict__ kb, const bf16x8* qreg, f32x16* sacc,
                                         int kbase) {
   using T = Tile<D>;
-  constexpr int KS = D / 16;
+  constexpr int NS = 2 * (D / 16);       // MFMAs per tile: 2 key halves x D/16 k-steps
+  constexpr int AHEAD = 4;
+  bf16x8 ka[NS];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) ka[i] = *(const bf16x8*)(kb + kbase + (i & 1) * 32 * T::KSTRIDE + 32 * (i >> 1));
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) sacc[kt][i] = 0.f;
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
+  for (int i = 0; i < NS; ++i) sacc[i & 1] = mfma32(ka[i], qreg[i >> 1], sacc[i & 1]);
+  __builtin_amdgcn_sched_group_barrier(kSgDsRead, AHEAD, 0);
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      const bf16x8 a = *(const bf16x8*)(kb + kbase + kt * 32 * T::KSTRIDE + 32 * ks);
-      sacc[kt] = mfma32(a, qreg[ks], sacc[kt]);
-    }
+  for (int i = 0; i < NS - AHEAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSgDsRead, 1, 0);
   }
+  __builtin_amdgcn_sched_group_barrier(kSgMfma, AHEAD, 0);
+}
+
+// O^T += V^T P^T for one 64-key tile (P in four bf16 B operands of 16 keys each).  The two
+// transpose reads of each V^T operand run two MFMAs ahead of their use.
+template <int D>
+__device__ __forceinline__ void pv_tile(const unsigned char* __restrict__ vb, const bf16x8* pb, f32x16* oacc,
+                                        int vbase) {
+  using T = Tile<D>;
+  constexpr int DT = D / 32;
+  constexpr int NM = 4 * DT;             // MFMAs per tile
+  constexpr int AHEAD = 2;
+  bf16x8 va[NM];
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    const int s4 = i / DT, dt = i % DT;
+    const unsigned char* vp = vb + vbase + (16 * s4) * T::VSTRIDE + 64 * dt;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(vp));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(vp + 8 * T::VSTRIDE));
+    const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    va[i] = __builtin_bit_cast(bf16x8, a8);
+  }
+#pragma unroll
+  for (int i = 0; i < NM; ++i) oacc[i % DT] = mfma32(va[i], pb[i / DT], oacc[i % DT]);
+  __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2 * AHEAD, 0);
+#pragma unroll
+  for (int i = 0; i < NM - AHEAD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kSgMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSgDsRead, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(kSgMfma, AHEAD, 0);
 }
 
 // Masks (ragged tail, frame-causal pairs), running max and the lazy rescale of O for one tile.
-// Lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row.
+// Lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row (column l%32); the
+// two lanes l and l^32 together hold the row's 64 keys.
 template <int D>
 __device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& m_run, float& l_run, int key0,
                                              const WaveCtx& w) {
@@ -156,7 +233,10 @@ __device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& 
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  // lanes l and l^32: the swap gives every lane both halves' values
+  const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, mx), __builtin_bit_cast(uint32_t, mx),
+                                                   false, false);
+  mx = fmaxf(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
   const float mt = mx * w.scale_log2;
   const bool raise = mt > m_run + kRescaleSlack;
   if (__any(raise)) {
@@ -171,13 +251,10 @@ __device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& 
   }
 }
 
-// P = 2^(S*scale - m) (row sums in fp32, P rounded to bf16 for the product), then
-// O^T += V^T P^T with the V^T operand read by LDS transpose loads.
-template <int D>
-__device__ __forceinline__ void softmax_pv(const f32x16* sacc, const unsigned char* __restrict__ vb, f32x16* oacc,
-                                           float m_run, float& l_run, const WaveCtx& w) {
-  using T = Tile<D>;
-  constexpr int DT = D / 32;
+// P = 2^(S*scale - m) rounded to bf16 into the four B operands of the P.V product; the row
+// sums are taken in fp32 before rounding.
+__device__ __forceinline__ void softmax_p(const f32x16* sacc, bf16x8* pb, float m_run, float& l_run,
+                                          float scale_log2) {
   const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
   float rs0 = 0.f, rs1 = 0.f;
 #pragma unroll
@@ -185,33 +262,23 @@ __device__ __forceinline__ void softmax_pv(const f32x16* sacc, const unsigned ch
     u32x4 pw;
 #pragma unroll
     for (int j2 = 0; j2 < 4; ++j2) {
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s4 >> 1][8 * (s4 & 1) + 2 * j2], w.scale_log2, -m_use));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s4 >> 1][8 * (s4 & 1) + 2 * j2 + 1], w.scale_log2, -m_use));
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s4 >> 1][8 * (s4 & 1) + 2 * j2], scale_log2, -m_use));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[s4 >> 1][8 * (s4 & 1) + 2 * j2 + 1], scale_log2, -m_use));
       pw[j2] = pack_bf16x2(p0, p1);
       rs0 += p0;
       rs1 += p1;
     }
-    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const unsigned char* va = vb + w.vbase + (16 * s4) * T::VSTRIDE + 64 * dt;
-      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va));
-      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(va + 8 * T::VSTRIDE));
-      const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      oacc[dt] = mfma32(__builtin_bit_cast(bf16x8, a8), pb, oacc[dt]);
-    }
+    pb[s4] = __builtin_bit_cast(bf16x8, pw);
   }
   l_run += rs0 + rs1;
 }
 
 // ---------------------------------------------------------------------------
-// Work plan.  A unit is 128 consecutive query rows of one (batch, head): two query blocks of
-// 64 rows or one of 128 (list 0 = first block, list 1 = second).  Its tiles are the 64-key
-// sub-tiles of the union of its kept lists, in ascending block order; entry = block << 4 |
-// ownership bits (bit L: list L keeps the block).  A unit with no kept block still gets one
-// (unowned) tile so that some workgroup writes its output.
-
-constexpr int kPersist = 512;    // persistent workgroups: two per CU on a 256-CU MI355X
+// Work plan.  Unit u = (bh, rt) covers query rows [256 rt, 256 rt + 256) of (batch, head) bh,
+// i.e. query blocks q0 .. q0 + NL - 1 with q0 = rt * NL and NL = 256 / block (list L = block
+// q0 + L).  Its tiles are the 64-key sub-tiles of the union of its lists in ascending block
+// order; entry = block << 4 | ownership bits (bit L: list L keeps the block).  A unit with no
+// kept block still gets one (unowned) tile so that some workgroup writes its output.
 
 __device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -233,31 +300,35 @@ __device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
   return base + incl - x;
 }
 
-__global__ __launch_bounds__(kThreads) void plan_union_kernel(const int32_t* __restrict__ counts,
-                                                              const int32_t* __restrict__ idx, int NQ, int NK,
-                                                              int block, int row_tiles, int32_t* __restrict__ ulist,
-                                                              int32_t* __restrict__ ucount) {
+constexpr int kPlanThreads = 256;
+
+__global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t* __restrict__ counts,
+                                                                  const int32_t* __restrict__ idx, int NQ, int NK,
+                                                                  int block, int row_tiles,
+                                                                  int32_t* __restrict__ ulist,
+                                                                  int32_t* __restrict__ ucount) {
   extern __shared__ __align__(16) uint32_t own[];     // 4 ownership bits per key block
-  __shared__ int sh[kThreads / 64];
+  __shared__ int sh[kPlanThreads / 64];
   const int u = blockIdx.x;
   const int bh = u / row_tiles, rt = u % row_tiles;
   const int tid = threadIdx.x;
   const int nwords = (NK + 7) >> 3;
-  for (int i = tid; i < nwords; i += kThreads) own[i] = 0;
+  for (int i = tid; i < nwords; i += kPlanThreads) own[i] = 0;
   __syncthreads();
-  const int q0 = rt * QR / block;
-  const int nlists = (block == 64 && q0 + 1 < NQ) ? 2 : 1;
+  const int NL = QR / block;
+  const int q0 = rt * NL;
+  const int nlists = min(NL, NQ - q0);
   for (int L = 0; L < nlists; ++L) {
     const size_t row = (size_t)bh * NQ + q0 + L;
     const int n = min(max(counts[row], 0), NK);
     const int32_t* lst = idx + row * NK;
-    for (int i = tid; i < n; i += kThreads) {
+    for (int i = tid; i < n; i += kPlanThreads) {
       const int j = lst[i];
       if ((unsigned)j < (unsigned)NK) atomicOr(&own[j >> 3], (1u << L) << ((j & 7) * 4));
     }
   }
   __syncthreads();
-  const int per = (nwords + kThreads - 1) / kThreads;
+  const int per = (nwords + kPlanThreads - 1) / kPlanThreads;
   const int w0 = min(tid * per, nwords), w1 = min(w0 + per, nwords);
   int cnt = 0;
   for (int wi = w0; wi < w1; ++wi) {
@@ -308,66 +379,215 @@ __global__ __launch_bounds__(1024) void plan_scan_kernel(const int32_t* __restri
   if (tid == 0) tstart[U] = carry;
 }
 
+// Expands every unit's union list into one record per 64-key tile at its place tstart[u] in the
+// global tile sequence (an empty unit gets one unowned record).
+__global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t* __restrict__ ulist,
+                                                                  const int32_t* __restrict__ ucount,
+                                                                  const int64_t* __restrict__ tstart, int NK,
+                                                                  int nsub, int block, int row_tiles,
+                                                                  int4* __restrict__ trec) {
+  const int u = blockIdx.x;
+  const int nb = ucount[u];
+  const int n = nb > 0 ? nb * nsub : 1;
+  const int bh = u / row_tiles, rt = u % row_tiles;
+  int4* out = trec + tstart[u];
+  for (int a = threadIdx.x; a < n; a += kPlanThreads) {
+    int key0 = 0, bits = 0;
+    if (nb > 0) {
+      const int e = ulist[(size_t)u * NK + (nsub == 2 ? (a >> 1) : a)];
+      key0 = (e >> 4) * block + (nsub == 2 ? (a & 1) * KT : 0);
+      bits = e & 15;
+    }
+    out[a] = int4{key0, bh, rt, bits | (a == 0 ? kFlFrom0 : 0) | (a == n - 1 ? kFlToEnd : 0)};
+  }
+}
+
 // Persistent workgroup lambda covers tiles [T lambda / P, T (lambda + 1) / P) of the global
 // tile sequence.
 __device__ inline int64_t range_begin(int64_t T, int lambda, int P) { return T * lambda / P; }
 
-// One step of the double-buffered loop for tile i (staged in kcur, vcur); tile i+1 is issued
-// into (knext, vnext) while i is multiplied.  The read and write buffers are distinct
-// __shared__ arrays, so the compiler can see that reads never wait on the asynchronous writes.
+// Per-tile record written by the planner: x = first key, y = (batch, head), z = row tile of
+// the unit, w = ownership bits (0..3) | from0 << 4 | to_end << 5, where from0 / to_end mark the
+// unit's first / last tile.
+
+// One tile of a workgroup's range (wave-uniform).  fl adds to the record's bits: first / last
+// tile of a piece (the unit's tiles inside this range), valid (inside the range).
 struct TileRef {
-  int key0;
-  int bits;
-  bool valid;
+  int key0, bh, rt, fl;
+  __device__ bool valid() const { return fl & kFlValid; }
+  __device__ bool owned(int list) const { return (fl >> list) & 1; }
 };
 
-template <int D>
-__device__ __forceinline__ void tile_step(const unsigned char* __restrict__ kcur, const unsigned char* __restrict__ vcur,
-                                          unsigned char* __restrict__ knext, unsigned char* __restrict__ vnext,
-                                          const TileRef& t0, const TileRef& t1, const uint16_t* kh,
-                                          const uint16_t* vh, const uint32_t* koff, const uint32_t* voff, int wave,
-                                          int my_list, bool wave_rows, const bf16x8* qreg, f32x16* oacc,
-                                          float& m_run, float& l_run, const WaveCtx& w) {
-  using T = Tile<D>;
-  // this thread's loads of (kcur, vcur) are done; the barrier makes every thread's loads
-  // visible and guarantees no wave still reads (knext, vnext), which held tile i-1
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (t1.valid) {
-    issue_rows<D, T::KINST, T::KPER>(knext, kh, t1.key0, w.key_lk, koff, wave);
-    issue_rows<D, T::VINST, T::VPER>(vnext, vh, t1.key0, w.key_lk, voff, wave);
+__device__ inline TileRef fetch_tile(const int4* __restrict__ trec, int64_t t, int64_t t_begin, int64_t t_end) {
+  TileRef r{0, 0, 0, 0};
+  if (t < t_end) {
+    const int4 e = trec[t];
+    r.key0 = e.x;
+    r.bh = e.y;
+    r.rt = e.z;
+    r.fl = e.w | kFlValid | ((e.w & kFlFrom0) || t == t_begin ? kFlFirst : 0) |
+           ((e.w & kFlToEnd) || t + 1 == t_end ? kFlLast : 0);
   }
-  if (((t0.bits >> my_list) & 1) && wave_rows) {
-    f32x16 sacc[2];
-    qk_tile<D>(kcur, qreg, sacc, w.kbase);
-    softmax_prep<D>(sacc, oacc, m_run, l_run, t0.key0, w);
-    softmax_pv<D>(sacc, vcur, oacc, m_run, l_run, w);
+  return r;
+}
+
+// State of one wave's running unit piece.
+template <int D>
+struct WaveState {
+  f32x16 oacc[D / 32];
+  f32x16 sacc[2];
+  bf16x8 pb[4];
+  bf16x8 qreg[D / 16];
+  float m_run, l_run;
+  bool rows;        // the wave's rows exist (r0w < Lq)
+  bool from0;       // the running piece starts at its unit's first tile
+  int r0w;          // first query row of the wave in its (batch, head)
+  int bh;
+};
+
+// Shared arguments of the phases.
+struct KArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;
+  float* part_o;
+  float* part_m;
+  float* part_l;
+  Geom gm;
+  int row_tiles;
+  int lambda;
+  int my_list;
+  int r_off;
+  int c32, h;
+};
+
+// Starts a piece of the unit of tile t: zero O, reset the running max and sum, load the wave's
+// Q rows.
+template <int D>
+__device__ __forceinline__ void start_piece(WaveState<D>& st, WaveCtx& w, const TileRef& t, const KArgs& ka) {
+  constexpr int KS = D / 16, DT = D / 32;
+  const Geom& gm = ka.gm;
+  st.bh = t.bh;
+  st.r0w = t.rt * QR + ka.r_off;
+  st.rows = st.r0w < gm.Lq;
+  st.from0 = t.fl & kFlFrom0;
+  st.m_run = -INFINITY;
+  st.l_run = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) st.oacc[dt][i] = 0.f;
+  // Q^T operand (32x32x16 B): lane holds Q[row r0w + l%32][16 ks + 8 (l/32) .. + 7]
+  const int row = st.r0w + ka.c32;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    u32x4 qw = u32x4{0u, 0u, 0u, 0u};
+    if (row < gm.Lq) qw = *(const u32x4*)(ka.q + ((size_t)st.bh * gm.Lq + row) * D + 16 * ks + 8 * ka.h);
+    st.qreg[ks] = __builtin_bit_cast(bf16x8, qw);
+  }
+  // complete the Q loads here: left pending, they would make every later Q.K^T (reached also
+  // without a piece start) wait for all vector memory traffic, the tile loads in flight included
+  __builtin_amdgcn_s_waitcnt(0);
+  // Key n is visible to query row t when n < Lk and, with frames of F tokens inside the chunk,
+  // when its chunk frame is not later than t's: n < chunk0 + (t / F + 1) F (context keys,
+  // n < chunk0, always pass).  One limit per lane replaces per-key frame arithmetic.
+  const int64_t lim = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)row / gm.F + 1) * gm.F : (int64_t)gm.Lk;
+  const int64_t limw = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)st.r0w / gm.F + 1) * gm.F : (int64_t)gm.Lk;
+  w.klimit = (int)(lim < gm.Lk ? lim : gm.Lk);
+  w.klimit_wave = (int)(limw < gm.Lk ? limw : gm.Lk);
+}
+
+// Ends a piece: the normalised bf16 output (and lse) when the piece is the whole unit, else the
+// fp32 partial (O unnormalised, running max m, sum l) in slot 2 lambda (the range's first piece,
+// which continues an earlier range) or 2 lambda + 1 (its last, continued by a later range).
+template <int D>
+__device__ __forceinline__ void end_piece(const WaveState<D>& st, bool to_end, const KArgs& ka) {
+  constexpr int DT = D / 32;
+  const Geom& gm = ka.gm;
+  const int c32 = ka.c32, h = ka.h;
+  // lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32]
+  const float l = st.l_run + __shfl_xor(st.l_run, 32);
+  const int qrow = st.r0w + c32;
+  if (qrow >= gm.Lq) return;
+  if (st.from0 && to_end) {
+    const float inv = l > 0.f ? 1.0f / l : 0.f;
+    uint16_t* orow = ka.o + ((size_t)st.bh * gm.Lq + qrow) * D + 4 * h;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        u32x2 ow;
+        ow[0] = pack_bf16x2(st.oacc[dt][4 * a4] * inv, st.oacc[dt][4 * a4 + 1] * inv);
+        ow[1] = pack_bf16x2(st.oacc[dt][4 * a4 + 2] * inv, st.oacc[dt][4 * a4 + 3] * inv);
+        *(u32x2*)(orow + 32 * dt + 8 * a4) = ow;
+      }
+    if (ka.lse && h == 0)
+      ka.lse[(size_t)st.bh * gm.Lq + qrow] = l > 0.f ? (st.m_run + log2f(l)) * 0.69314718055994531f : -INFINITY;
+  } else {
+    const int slot = 2 * ka.lambda + (st.from0 ? 1 : 0);
+    const size_t prow = (size_t)slot * QR + ka.r_off + c32;
+    float* po = ka.part_o + prow * D + 4 * h;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4)
+        *(f32x4*)(po + 32 * dt + 8 * a4) =
+            f32x4{st.oacc[dt][4 * a4], st.oacc[dt][4 * a4 + 1], st.oacc[dt][4 * a4 + 2], st.oacc[dt][4 * a4 + 3]};
+    if (h == 0) {
+      ka.part_m[prow] = st.m_run;
+      ka.part_l[prow] = l;
+    }
   }
 }
 
-__device__ inline TileRef tile_ref(const int32_t* __restrict__ ul, int64_t i, int64_t n, int nsub, int block,
-                                   int nblocks) {
-  TileRef t;
-  t.valid = i < n;
-  t.key0 = 0;
-  t.bits = 0;
-  if (t.valid && nblocks > 0) {
-    const int e = ul[nsub == 2 ? (i >> 1) : i];
-    t.key0 = (e >> 4) * block + (nsub == 2 ? (int)(i & 1) * KT : 0);
-    t.bits = e & 15;
+// M phase of tile `cur` (previous tile `prev`): P.V of prev, end of prev's piece, start of
+// cur's piece, Q.K^T of cur.
+template <int D>
+__device__ __forceinline__ void m_phase(WaveState<D>& st, WaveCtx& w, const TileRef& prev, const TileRef& cur,
+                                        const unsigned char* kcur, const unsigned char* vprev, const KArgs& ka) {
+  if (prev.valid()) {
+    if (prev.owned(ka.my_list) && st.rows) pv_tile<D>(vprev, st.pb, st.oacc, w.vbase);
+    if (prev.fl & kFlLast) end_piece<D>(st, prev.fl & kFlToEnd, ka);
   }
-  return t;
+  if (cur.valid()) {
+    if (cur.fl & kFlFirst) start_piece<D>(st, w, cur, ka);
+    if (cur.owned(ka.my_list) && st.rows) qk_tile<D>(kcur, st.qreg, st.sacc, w.kbase);
+  }
+}
+
+// V phase of tile `cur`: masks, running max, rescale, P.
+template <int D>
+__device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, const TileRef& cur, const KArgs& ka) {
+  if (cur.valid() && cur.owned(ka.my_list) && st.rows) {
+    softmax_prep<D>(st.sacc, st.oacc, st.m_run, st.l_run, cur.key0, w);
+    softmax_p(st.sacc, st.pb, st.m_run, st.l_run, w.scale_log2);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void issue_tile_loads(unsigned char* kdst, unsigned char* vdst, const TileRef& tk,
+                                                 const TileRef& tv, const KArgs& ka, const uint32_t* koff,
+                                                 const uint32_t* voff, int lw) {
+  using T = Tile<D>;
+  if (tk.valid()) {
+    const uint16_t* kh = ka.k + (size_t)tk.bh * ka.gm.Lk * D;
+    issue_rows<D, T::KINST, T::KPER>(kdst, kh, tk.key0, ka.gm.Lk, koff, lw);
+  }
+  if (tv.valid()) {
+    const uint16_t* vh = ka.v + (size_t)tv.bh * ka.gm.Lk * D;
+    issue_rows<D, T::VINST, T::VPER>(vdst, vh, tv.key0, ka.gm.Lk, voff, lw);
+  }
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const int32_t* __restrict__ ulist, const int32_t* __restrict__ ucount, const int64_t* __restrict__ tstart,
-    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
-    float* __restrict__ part_l, Geom gm, int BH, int row_tiles, int U, float scale_log2) {
+    const int4* __restrict__ trec, const int64_t* __restrict__ tstart, uint16_t* __restrict__ o,
+    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m, float* __restrict__ part_l,
+    Geom gm, int row_tiles, int U, float scale_log2) {
   using T = Tile<D>;
-  constexpr int KS = D / 16;   // k-steps of Q.K^T (32x32x16)
-  constexpr int DT = D / 32;   // d tiles of P.V
   __shared__ __attribute__((aligned(1024))) unsigned char kbuf0[T::KBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char kbuf1[T::KBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char vbuf0[T::VBYTES];
@@ -375,37 +595,53 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   // XCD-aware range: hardware places consecutive workgroup ids on consecutive XCDs (round
   // robin over 8); the workgroups of one XCD get consecutive ranges, i.e. consecutive units
-  // of the same heads, so each L2 keeps its heads' shared K/V.
+  // of the same heads, so each L2 keeps its heads' shared K/V.  P is a multiple of 8.
   const int P = gridDim.x;
   const int lambda = (blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3);
   const int64_t Ttot = tstart[U];
   const int64_t t_begin = range_begin(Ttot, lambda, P), t_end = range_begin(Ttot, lambda + 1, P);
   if (t_begin >= t_end) return;
-  // unit holding t_begin: largest u with tstart[u] <= t_begin
-  int ulo = 0, uhi = U - 1;
-  while (ulo < uhi) {
-    const int mid = (ulo + uhi + 1) >> 1;
-    if (tstart[mid] <= t_begin) ulo = mid;
-    else uhi = mid - 1;
-  }
-  int u = ulo;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps tile-issue math scalar
+  const bool g1 = wave >= 4;                                    // the lagging group, which also loads
+  const int lw = wave & 3;
   const int c32 = lane & 31, h = lane >> 5;
-  const int nsub = gm.block / KT;
-  const int my_list = (gm.block == 64 && wave >= 2) ? 1 : 0;   // waves 2, 3 own the second block
 
-  // lane-constant global offsets of this wave's tile loads
+  KArgs ka;
+  ka.q = q;
+  ka.k = k;
+  ka.v = v;
+  ka.o = o;
+  ka.lse = lse;
+  ka.part_o = part_o;
+  ka.part_m = part_m;
+  ka.part_l = part_l;
+  ka.gm = gm;
+  ka.row_tiles = row_tiles;
+  ka.lambda = lambda;
+  ka.c32 = c32;
+  ka.h = h;
+  // the two waves of SIMD s (s and s + 4) own the two 32-row halves of one 64-row query block,
+  // or (128-row blocks) waves {0, 1, 4, 5} and {2, 3, 6, 7} own the two blocks
+  if (gm.block == 64) {
+    ka.my_list = wave & 3;
+    ka.r_off = (wave & 3) * 64 + (wave >> 2) * QW;
+  } else {
+    ka.my_list = (wave & 3) >> 1;
+    ka.r_off = ka.my_list * 128 + ((wave & 1) * 2 + (wave >> 2)) * QW;
+  }
+
+  // lane-constant global offsets of this wave's tile loads (group 1 only)
   uint32_t koff[T::KPER], voff[T::VPER];
 #pragma unroll
   for (int uu = 0; uu < T::KPER; ++uu) {
-    const int n = wave + 4 * uu;
+    const int n = lw + 4 * uu;
     koff[uu] = n < T::KINST ? slot_offset<D>(n, lane, T::KSLOTS) : 0x7fffffffu;
   }
 #pragma unroll
   for (int uu = 0; uu < T::VPER; ++uu) {
-    const int n = wave + 4 * uu;
+    const int n = lw + 4 * uu;
     voff[uu] = n < T::VINST ? slot_offset<D>(n, lane, T::VSLOTS) : 0x7fffffffu;
   }
   WaveCtx w;
@@ -414,130 +650,81 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   w.vbase = (4 * h + ((lane & 15) >> 2)) * T::VSTRIDE + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
   w.h = h;
   w.scale_log2 = scale_log2;
+  w.klimit = gm.Lk;
+  w.klimit_wave = gm.Lk;
 
-  int64_t t = t_begin;
-  while (t < t_end) {
-    const int64_t ts = tstart[u], te = tstart[u + 1];
-    const int64_t a = t - ts, b = (te < t_end ? te : t_end) - ts;   // local tile range [a, b)
-    const bool full = (a == 0) && (b == te - ts);
-    const int bh = u / row_tiles, rt = u % row_tiles;
-    const int row_base = rt * QR;
-    const int r0w = row_base + wave * QW;               // first query row of this wave
-    const bool wave_rows = r0w < gm.Lq;
-    const int nblocks = ucount[u];
-    const int32_t* ul = ulist + (size_t)u * gm.NK;
-    const int64_t ntiles = (int64_t)nblocks * nsub;     // 0 for an empty unit (its dummy tile is unowned)
-    const uint16_t* kh = k + (size_t)bh * gm.Lk * D;
-    const uint16_t* vh = v + (size_t)bh * gm.Lk * D;
+  WaveState<D> st;
+  st.m_run = -INFINITY;
+  st.l_run = 0.f;
+  st.rows = false;
+  st.from0 = false;
+  st.r0w = 0;
+  st.bh = 0;
 
-    // Q^T operand (32x32x16 B): lane holds Q[row r0w + l%32][16 ks + 8 (l/32) .. + 7]
-    bf16x8 qreg[KS];
-    {
-      const int row = r0w + c32;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u32x4 qw = u32x4{0u, 0u, 0u, 0u};
-        if (row < gm.Lq) qw = *(const u32x4*)(q + ((size_t)bh * gm.Lq + row) * D + 16 * ks + 8 * h);
-        qreg[ks] = __builtin_bit_cast(bf16x8, qw);
-      }
-    }
-    // Key n is visible to query row t when n < Lk and, with frames of F tokens inside the chunk,
-    // when its chunk frame is not later than t's: n < chunk0 + (t / F + 1) F (context keys,
-    // n < chunk0, always pass).  One limit per lane replaces per-key frame arithmetic.
-    {
-      const int64_t lim = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)(r0w + c32) / gm.F + 1) * gm.F : (int64_t)gm.Lk;
-      const int64_t limw = gm.F > 0 ? (int64_t)gm.chunk0 + ((int64_t)r0w / gm.F + 1) * gm.F : (int64_t)gm.Lk;
-      w.klimit = (int)(lim < gm.Lk ? lim : gm.Lk);
-      w.klimit_wave = (int)(limw < gm.Lk ? limw : gm.Lk);
-    }
-    f32x16 oacc[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
-    float m_run = -INFINITY;
-    float l_run = 0.f;
+  const int64_t N = t_end - t_begin;
+  TileRef prev{0, 0, 0, 0};
+  TileRef cur = fetch_tile(trec, t_begin, t_begin, t_end);
+  TileRef nxt = fetch_tile(trec, t_begin + 1, t_begin, t_end);
 
-    const int64_t bb = b < ntiles ? b : ntiles;         // real tiles of this piece (dummy tile: none)
-    // previous unit's last tile may still be read from either buffer: sync before refilling
-    __syncthreads();
-    TileRef t0 = tile_ref(ul, a, bb, nsub, gm.block, nblocks);
-    TileRef t1 = tile_ref(ul, a + 1, bb, nsub, gm.block, nblocks);
-    if (t0.valid) {
-      issue_rows<D, T::KINST, T::KPER>(kbuf0, kh, t0.key0, gm.Lk, koff, wave);
-      issue_rows<D, T::VINST, T::VPER>(vbuf0, vh, t0.key0, gm.Lk, voff, wave);
-    }
-    int64_t i = a;
-    while (t0.valid) {
-      tile_step<D>(kbuf0, vbuf0, kbuf1, vbuf1, t0, t1, kh, vh, koff, voff, wave, my_list, wave_rows, qreg, oacc,
-                   m_run, l_run, w);
-      ++i;
-      t0 = t1;
-      t1 = tile_ref(ul, i + 1, bb, nsub, gm.block, nblocks);
-      if (!t0.valid) break;
-      tile_step<D>(kbuf1, vbuf1, kbuf0, vbuf0, t0, t1, kh, vh, koff, voff, wave, my_list, wave_rows, qreg, oacc,
-                   m_run, l_run, w);
-      ++i;
-      t0 = t1;
-      t1 = tile_ref(ul, i + 1, bb, nsub, gm.block, nblocks);
-    }
-    // no load is left in flight: the last step issued nothing (its next tile was invalid)
-
-    // ---- output: lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32] ----
-    const float l = l_run + __shfl_xor(l_run, 32);
-    const int qrow = r0w + c32;
-    if (qrow < gm.Lq) {
-      if (full) {
-        const float inv = l > 0.f ? 1.0f / l : 0.f;
-        uint16_t* orow = o + ((size_t)bh * gm.Lq + qrow) * D + 4 * h;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int a4 = 0; a4 < 4; ++a4) {
-            u32x2 ow;
-            ow[0] = pack_bf16x2(oacc[dt][4 * a4] * inv, oacc[dt][4 * a4 + 1] * inv);
-            ow[1] = pack_bf16x2(oacc[dt][4 * a4 + 2] * inv, oacc[dt][4 * a4 + 3] * inv);
-            *(u32x2*)(orow + 32 * dt + 8 * a4) = ow;
-          }
-        if (lse && h == 0)
-          lse[(size_t)bh * gm.Lq + qrow] = l > 0.f ? (m_run + log2f(l)) * 0.69314718055994531f : -INFINITY;
-      } else {
-        // a piece of a unit split across workgroups: the workgroup's first unit goes to slot
-        // 2 lambda, its last (when it continues past the range) to slot 2 lambda + 1
-        const int slot = 2 * lambda + (a > 0 ? 0 : 1);
-        const size_t prow = (size_t)slot * QR + (qrow - row_base);
-        float* po = part_o + prow * D + 4 * h;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int a4 = 0; a4 < 4; ++a4)
-            *(f32x4*)(po + 32 * dt + 8 * a4) =
-                f32x4{oacc[dt][4 * a4], oacc[dt][4 * a4 + 1], oacc[dt][4 * a4 + 2], oacc[dt][4 * a4 + 3]};
-        if (h == 0) {
-          part_m[prow] = m_run;
-          part_l[prow] = l;
-        }
-      }
-    }
-    t = ts + b;
-    ++u;
+  // prologue: K of the first tile
+  if (g1) {
+    const TileRef none{0, 0, 0, 0};
+    issue_tile_loads<D>(kbuf0, vbuf0, cur, none, ka, koff, voff, lw);
+    __builtin_amdgcn_s_waitcnt(0);
   }
+  lds_barrier();
+
+  auto run = [&](auto G1) {
+    constexpr bool IS_G1 = decltype(G1)::value;
+    auto iteration = [&](unsigned char* kc, unsigned char* kn, unsigned char* vc, unsigned char* vp) {
+      if constexpr (!IS_G1) {
+        m_phase<D>(st, w, prev, cur, kc, vp, ka);
+        lds_barrier();
+        v_phase<D>(st, w, cur, ka);
+        lds_barrier();
+      } else {
+        v_phase<D>(st, w, prev, ka);
+        issue_tile_loads<D>(kn, vc, nxt, cur, ka, koff, voff, lw);
+        barrier_keep_loads();
+        m_phase<D>(st, w, prev, cur, kc, vp, ka);
+        __builtin_amdgcn_s_waitcnt(0);
+        lds_barrier();
+      }
+    };
+    for (int64_t hh = 0; hh <= N; hh += 2) {
+      iteration(kbuf0, kbuf1, vbuf0, vbuf1);
+      prev = cur;
+      cur = nxt;
+      nxt = fetch_tile(trec, t_begin + hh + 2, t_begin, t_end);
+      if (hh + 1 > N) break;
+      iteration(kbuf1, kbuf0, vbuf1, vbuf0);
+      prev = cur;
+      cur = nxt;
+      nxt = fetch_tile(trec, t_begin + hh + 3, t_begin, t_end);
+    }
+  };
+  if (g1) run(std::true_type{});
+  else run(std::false_type{});
+  // every load was waited for inside the loop (the last iterations issue none)
 }
 
 // Merges the pieces of units that were split across workgroups:
 // O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s, over the pieces in workgroup order
-// (deterministic).  Thread t owns 4 columns and QR * D / (4 * kThreads) rows of the unit, so
-// the loads of all its rows are in flight together.
+// (deterministic).  Thread t owns 4 columns and QR * D / (4 * kCombThreads) rows of the unit,
+// so the loads of all its rows are in flight together.
+constexpr int kCombThreads = 512;
+
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_combine_kernel(const int64_t* __restrict__ tstart, int U, int P,
-                                                                int row_tiles, int Lq,
-                                                                const float* __restrict__ part_o,
-                                                                const float* __restrict__ part_m,
-                                                                const float* __restrict__ part_l,
-                                                                uint16_t* __restrict__ o, float* __restrict__ lse) {
-  constexpr int CG = D / 4;                 // 4-column groups per row
-  constexpr int RSTEP = kThreads / CG;      // rows per pass
-  constexpr int NI = QR / RSTEP;            // rows per thread
+__global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int64_t* __restrict__ tstart, int U, int P,
+                                                                    int row_tiles, int Lq,
+                                                                    const float* __restrict__ part_o,
+                                                                    const float* __restrict__ part_m,
+                                                                    const float* __restrict__ part_l,
+                                                                    uint16_t* __restrict__ o,
+                                                                    float* __restrict__ lse) {
+  constexpr int CG = D / 4;                    // 4-column groups per row
+  constexpr int RSTEP = kCombThreads / CG;     // rows per pass
+  constexpr int NI = QR / RSTEP;               // rows per thread
   const int u = blockIdx.x;
   const int64_t Ttot = tstart[U], ts = tstart[u], te = tstart[u + 1];
   // workgroup (range) holding tile t: largest lambda with T lambda / P <= t
@@ -592,6 +779,7 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(const int64_t* _
 }
 
 struct AttnWs {
+  int4* trec;
   int32_t* ulist;
   int32_t* ucount;
   int64_t* tstart;
@@ -604,10 +792,13 @@ struct AttnWs {
 AttnWs attn_ws_layout(const Dims& dm, void* base) {
   const int row_tiles = ceil_div(dm.Lq, QR);
   const size_t U = (size_t)dm.BH * row_tiles;
-  const size_t slots = 2 * (size_t)kPersist;
+  const size_t slots = 2 * (size_t)kMaxPersist;
   size_t off = 0;
   AttnWs w;
   char* b = (char*)base;
+  // at most max(1, NK * nsub) tiles per unit
+  w.trec = (int4*)(b + off);
+  off += align256(U * (size_t)dm.NK * (dm.block / KT) * sizeof(int4));
   w.ulist = (int32_t*)(b + off);
   off += align256(U * dm.NK * sizeof(int32_t));
   w.ucount = (int32_t*)(b + off);
@@ -624,6 +815,17 @@ AttnWs attn_ws_layout(const Dims& dm, void* base) {
   return w;
 }
 
+// Persistent workgroups: one per CU of the current device, a multiple of 8 (XCD round robin),
+// at most kMaxPersist (the partial slots of the workspace are sized for that many).
+int persistent_workgroups() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 8)
+    cus = 8;
+  const int p = cus < kMaxPersist ? cus : kMaxPersist;
+  return p & ~7;
+}
+
 }  // namespace
 
 size_t attn_ws_bytes(const Dims& dm) { return attn_ws_layout(dm, nullptr).bytes; }
@@ -633,25 +835,28 @@ hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void*
   const int row_tiles = ceil_div(dm.Lq, QR);
   const int U = dm.BH * row_tiles;
   const int nsub = dm.block / KT;
+  const int P = persistent_workgroups();
   AttnWs w = attn_ws_layout(dm, ws);
   Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
   const float scale_log2 = scale * 1.4426950408889634f;
-  hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t), st,
-                     counts, idx, dm.NQ, dm.NK, dm.block, row_tiles, w.ulist, w.ucount);
+  hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
+                     st, counts, idx, dm.NQ, dm.NK, dm.block, row_tiles, w.ulist, w.ucount);
   hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(1024), 0, st, w.ucount, U, nsub, w.tstart);
+  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, w.tstart, dm.NK, nsub,
+                     dm.block, row_tiles, w.trec);
   if (dm.d == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(kPersist), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, w.ulist, w.ucount, w.tstart, (uint16_t*)o, lse,
-                       w.part_o, w.part_m, w.part_l, gm, dm.BH, row_tiles, U, scale_log2);
+    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
+                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, (uint16_t*)o, lse,
+                       w.part_o, w.part_m, w.part_l, gm, row_tiles, U, scale_log2);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(kPersist), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, w.ulist, w.ucount, w.tstart, (uint16_t*)o, lse,
-                       w.part_o, w.part_m, w.part_l, gm, dm.BH, row_tiles, U, scale_log2);
+    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
+                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, (uint16_t*)o, lse,
+                       w.part_o, w.part_m, w.part_l, gm, row_tiles, U, scale_log2);
   if (dm.d == 128)
-    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(U), dim3(kThreads), 0, st, w.tstart, U, kPersist, row_tiles,
+    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(U), dim3(kCombThreads), 0, st, w.tstart, U, P, row_tiles,
                        dm.Lq, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(U), dim3(kThreads), 0, st, w.tstart, U, kPersist, row_tiles,
+    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(U), dim3(kCombThreads), 0, st, w.tstart, U, P, row_tiles,
                        dm.Lq, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   return hipGetLastError();
 }
