@@ -65,7 +65,8 @@ typedef enum la_status {
  * Key block m is forced (always kept, never scored) when it overlaps the text
  * tokens [0, n_text) or the chunk [Lk - Lq, Lk); the others are the M historical
  * candidates, block indices [ceil(n_text/block), floor((Lk-Lq)/block)).
- * Limits: NK <= 16384, M <= 4096, B*H <= 65535. */
+ * Limits: NK <= 16384, M <= 4096, B*H <= 65535, and B*H*ceil(Lq/256)*NK*(block/64)
+ * < 2^31 (the 64-key tiles of the attention work plan have 32-bit indices). */
 typedef struct la_shape {
   int32_t B, H, Lq, Lk, d;
   int32_t block;

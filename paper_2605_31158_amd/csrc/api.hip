@@ -28,6 +28,10 @@ la_status make_dims(const la_shape* s, Dims* o) {
   if (o->h1 < o->h0) o->h1 = o->h0;
   o->M = o->h1 - o->h0;
   if (o->M > kMaxCandidates) return LA_ERR_SHAPE;
+  // the attention work plan numbers 64-key tiles with 32-bit indices: units of 256 query rows
+  // times at most NK * block / 64 tiles each
+  const int64_t units = (int64_t)o->BH * ceil_div(s->Lq, 256);
+  if (units * o->NK * (s->block / 64) >= (int64_t(1) << 31)) return LA_ERR_SHAPE;
   return LA_OK;
 }
 

@@ -2,32 +2,35 @@
 // one kept-block list per query block serving both K and V).
 //
 // Work decomposition
-//   * A unit is 256 consecutive query rows of one (batch, head): four query blocks of 64 rows
-//     or two of 128.  Its tiles are the 64-key sub-tiles of the union of its blocks' kept
-//     lists, in ascending key order, each tagged with which of the unit's blocks kept it.
-//   * A planner (three small kernels) builds every unit's union list, the prefix sum of the
-//     units' tile counts and one record per tile (first key, head, row tile, ownership).
-//     One persistent workgroup per CU then takes an equal share of the concatenated tile
-//     sequence (stream-K); a unit cut between two workgroups leaves
-//     (O, m, l) partials that attn_combine merges with a log-sum-exp merge.  Heavy query
-//     blocks therefore never bound the launch.
+//   * A unit is 256 query rows of one (batch, head): four query blocks of 64 rows or two of 128.
+//     Query blocks are grouped by the first historical key block they keep, so that blocks
+//     which chose the same context share a unit.  Its tiles are the 64-key sub-tiles of the
+//     union of its blocks' kept lists, in ascending key order, each tagged with which of the
+//     unit's blocks kept it.
+//   * A planner (three small kernels) computes the grouping keys, every unit's union list and
+//     one record per tile (first key, head, unit, ownership) in the concatenated tile sequence
+//     of all units.  One persistent workgroup per CU then takes an equal share of that sequence
+//     (stream-K); a unit cut between two workgroups leaves (O, m, l) partials that attn_combine
+//     merges with a log-sum-exp merge.  Heavy query blocks therefore never bound the launch.
 //   * Workgroup ranges are laid out so that the workgroups of one XCD hold consecutive units,
 //     i.e. the same heads: the shared chunk K/V of a head stays in that XCD's L2.
 //
 // The workgroup: 8 waves = two groups of four, one wave of each group per SIMD.  Each wave owns
 // 32 query rows; the two waves of a SIMD own the two halves of the same query block, so both
-// groups own the same tiles.  The groups run a ping-pong over the tile sequence, offset by one
-// phase and separated by workgroup barriers:
+// groups own the same tiles.  The groups alternate, offset by one phase and separated by
+// workgroup barriers:
 //
-//   phase    group 0                          group 1
-//   A(h)     M(h): P.V of tile h-1, Q.K^T h   V(h-1): softmax of tile h-1; load K(h+1), V(h)
-//   B(h)     V(h): softmax of tile h          M(h): P.V of tile h-1, Q.K^T of tile h
+//   phase    group 0                              group 1
+//   A(h)     M(h): P.V of tile h-1, Q.K^T of h    V(h-1): softmax of tile h-1, loads K(h+2)
+//   B(h)     V(h): softmax of tile h, loads V(h+1) M(h): P.V of tile h-1, Q.K^T of tile h
 //
 // so on every SIMD one wave feeds the matrix pipeline while the other does the softmax
-// arithmetic.  K and V tiles live in two-stage LDS rings each (K(h) is read in A(h) and B(h),
-// V(h) in A(h+1) and B(h+1)); group 1 issues the asynchronous buffer-to-LDS loads of K(h+1) and
-// V(h) in A(h) and waits for them at the end of B(h).  The loads' buffer descriptors end at Lk,
-// so the ragged last block reads zeros past the end.
+// arithmetic, and the asynchronous buffer-to-LDS tile loads are spread among that arithmetic
+// in both phases.  K and V live in three-stage LDS rings: K(h) is read in A(h) and B(h), V(h)
+// in A(h+1) and B(h+1), so K(h+2) and V(h+1) can be written from A(h) on.  A group waits for
+// the loads it issued one V phase earlier at the end of its next V phase (vmcnt: all but the
+// loads just issued).  The loads' buffer descriptors end at Lk, so the ragged last block reads
+// zeros past the end.
 //
 // Per wave and 64-key tile (d = 128):
 //   S^T (64 keys x 32 queries) = K_tile (64 x d) . Q^T       16 x v_mfma_f32_32x32x16_bf16
@@ -35,10 +38,8 @@
 //   max exceeds it by more than 2^8, so most tiles skip the rescale of O)
 //   O^T (d x 32) += V^T (d x 64) . P^T (64 x 32)              16 x v_mfma_f32_32x32x16_bf16
 // S^T is computed transposed so that its accumulator layout (each lane holds 16 keys of one
-// query column) is, 8 values at a time, directly the B operand of the P.V product.  K and V
-// tiles are row-major in LDS with padded rows; every operand read is a lane base address
-// plus a compile-time offset.  The V^T operand is read with the LDS transpose load
-// ds_read_b64_tr_b16 (two per MFMA).
+// query column) is, 8 values at a time, directly the B operand of the P.V product.  The V^T
+// operand is read with the LDS transpose load ds_read_b64_tr_b16 (two per MFMA).
 #include <math.h>
 
 #include <type_traits>
@@ -75,8 +76,7 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2v));
 }
 
-// Workgroup barrier that orders LDS accesses only: the asynchronous tile loads in flight
-// (tracked by vmcnt) are not waited for.
+// Workgroup barrier that orders LDS accesses (waits for this wave's LDS operations).
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
@@ -85,18 +85,27 @@ __device__ __forceinline__ void lds_barrier() {
 
 // Workgroup barrier for a wave with asynchronous tile loads in flight that it does not wait for
 // here: the LDS release fence of lds_barrier would wait for them (they write LDS).  The empty
-// asm statements keep the compiler from moving memory accesses across the barrier; the wave
-// has no LDS access of its own outstanding at this point.
+// asm statements keep the compiler from moving memory accesses across the barrier; every LDS
+// read of the wave has been consumed by then.
 __device__ __forceinline__ void barrier_keep_loads() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
 
+// Waits until at most n of this wave's vector memory operations are outstanding (n < 16).
+template <int n>
+__device__ __forceinline__ void wait_vmem() {
+  __builtin_amdgcn_s_waitcnt(0x0F70 | n);   // vmcnt(n), expcnt and lgkmcnt left at their maximum
+}
+
 // LDS layout: K and V tiles of 64 key rows of D bf16, row-major with padded rows.  K rows are
 // padded to D*2 + 16 bytes: the 32 key rows an MFMA operand read touches (16 per LDS cycle)
 // start in distinct 16-byte bank groups.  V rows are padded to D*2 + 64 bytes: a transpose
 // read touches 4 rows x 64 contiguous bytes per half-wave, which then cover all 64 banks once.
+// Every operand read is then a lane base address plus a compile-time offset.  A tile is
+// written by wave-wide 16-byte-per-lane loads (1 KiB each) of consecutive 16-byte slots;
+// padding slots read as zero.
 template <int D>
 struct Tile {
   static constexpr int KSTRIDE = D * 2 + 16;
@@ -105,10 +114,11 @@ struct Tile {
   static constexpr int VSLOTS = VSTRIDE / 16;
   static constexpr int KBYTES = KT * KSTRIDE;
   static constexpr int VBYTES = KT * VSTRIDE;
-  static constexpr int KINST = KT * KSLOTS / 64;       // wave-wide 1 KiB loads per K tile
-  static constexpr int VINST = KT * VSLOTS / 64;
-  static constexpr int KPER = (KINST + 3) / 4;         // per loading wave (4 waves load)
-  static constexpr int VPER = (VINST + 3) / 4;
+  static constexpr int KINST = KT * KSLOTS / 64;       // wave-wide loads per K tile: 4 KPER + 1
+  static constexpr int VINST = KT * VSLOTS / 64;       // per V tile: 4 VPER
+  static constexpr int KPER = KINST / 4;               // per loading wave (wave 0 loads one more)
+  static constexpr int VPER = VINST / 4;
+  static_assert(KINST % 4 == 1 && VINST % 4 == 0, "load split");
 };
 
 // Global byte offset (inside a tile of 64 rows) that lane `lane` of load `n` fetches so that it
@@ -121,22 +131,34 @@ __device__ inline uint32_t slot_offset(int n, int lane, int slots) {
   return chunk < D / 8 ? (uint32_t)(row * D * 2 + chunk * 16) : 0x7fffffffu;
 }
 
-// Issues this wave's share (loading wave lw of 4) of the buffer-to-LDS loads of one 64-key
-// tile of one matrix into `dst`.  The descriptor starts at the tile and ends at Lk: rows past
-// Lk and padding slots read as zero.
-template <int D, int NINST, int PER>
-__device__ inline void issue_rows(unsigned char* dst, const uint16_t* base, int key0, int Lk, const uint32_t* off,
-                                  int lw) {
-  // a tile may start at or past Lk (second half of a ragged 128-key block): no valid rows
-  const uint32_t nrec = key0 < Lk ? (uint32_t)(Lk - key0) * (uint32_t)(D * 2) : 0u;
-  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)key0 * D), 0, nrec, 0x00020000);
-#pragma unroll
-  for (int u = 0; u < PER; ++u) {
-    const int n = lw + 4 * u;
-    if (NINST % 4 == 0 || n < NINST)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void*)(dst + 1024 * n), 16, off[u], 0, 0, 0);
-  }
+// Loads of one tile of one matrix by one loading wave: a buffer descriptor that starts at the
+// tile and ends at Lk (rows past Lk read as zero; an invalid tile reads nothing) and the LDS
+// destination.  Load j fills LDS bytes [1024 (lw + 4 j), + 1024) of the tile.
+struct TileLoad {
+  __amdgpu_buffer_rsrc_t rsrc;
+  unsigned char* dst;
+};
+
+template <int D>
+__device__ inline TileLoad tile_load(unsigned char* dst, const uint16_t* base, int key0, int Lk, bool valid) {
+  const uint32_t nrec = valid && key0 < Lk ? (uint32_t)(Lk - key0) * (uint32_t)(D * 2) : 0u;
+  TileLoad t;
+  t.rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)(valid ? key0 : 0) * D), 0, nrec, 0x00020000);
+  t.dst = dst;
+  return t;
 }
+
+template <int NL>
+struct LoadSet {
+  TileLoad t;
+  int lw;
+  const uint32_t* off;      // off[j]: the lane's global offset for load j
+  __device__ __forceinline__ void issue(int j) const { issue_at(lw + 4 * j, off[j]); }
+  // load n of the tile with the lane offset o
+  __device__ __forceinline__ void issue_at(int n, uint32_t o) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rsrc, (LDS_AS void*)(t.dst + 1024 * n), 16, o, 0, 0, 0);
+  }
+};
 
 struct Geom {
   int Lq, Lk, block, NQ, NK, F, chunk0;
@@ -154,6 +176,8 @@ struct WaveCtx {
 
 // Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
 constexpr int kSgMfma = 0x008;
+constexpr int kSgValu = 0x002 | 0x400;   // VALU and transcendental
+constexpr int kSgVmemRead = 0x020;
 constexpr int kSgDsRead = 0x100;
 
 // S^T = K Q^T for one 64-key tile: two 32x32 accumulators (keys 0..31, 32..63).  The K operand
@@ -252,9 +276,13 @@ __device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& 
 }
 
 // P = 2^(S*scale - m) rounded to bf16 into the four B operands of the P.V product; the row
-// sums are taken in fp32 before rounding.
+// sums are taken in fp32 before rounding and added to l_run when `use` (a wave that does not
+// own the tile runs the same straight-line code on stale scores and drops the result).  The NL
+// tile loads of `ld` are spread among the arithmetic.
+template <int NL>
 __device__ __forceinline__ void softmax_p(const f32x16* sacc, bf16x8* pb, float m_run, float& l_run,
-                                          float scale_log2) {
+                                          float scale_log2, bool use, const LoadSet<NL>& ld) {
+  constexpr int NV = 112;                // VALU per tile: 32 fma + 32 exp + 32 add + 16 cvt
   const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
   float rs0 = 0.f, rs1 = 0.f;
 #pragma unroll
@@ -270,15 +298,50 @@ __device__ __forceinline__ void softmax_p(const f32x16* sacc, bf16x8* pb, float 
     }
     pb[s4] = __builtin_bit_cast(bf16x8, pw);
   }
-  l_run += rs0 + rs1;
+#pragma unroll
+  for (int j = 0; j < NL; ++j) ld.issue(j);
+  if constexpr (NL > 0) {
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      __builtin_amdgcn_sched_group_barrier(kSgValu, NV / (NL + 1), 0);
+      __builtin_amdgcn_sched_group_barrier(kSgVmemRead, 1, 0);
+    }
+  }
+  l_run += use ? rs0 + rs1 : 0.f;
 }
 
 // ---------------------------------------------------------------------------
-// Work plan.  Unit u = (bh, rt) covers query rows [256 rt, 256 rt + 256) of (batch, head) bh,
-// i.e. query blocks q0 .. q0 + NL - 1 with q0 = rt * NL and NL = 256 / block (list L = block
-// q0 + L).  Its tiles are the 64-key sub-tiles of the union of its lists in ascending block
-// order; entry = block << 4 | ownership bits (bit L: list L keeps the block).  A unit with no
-// kept block still gets one (unowned) tile so that some workgroup writes its output.
+// Work plan.  The query blocks of each (batch, head) bh are ordered by the first historical key
+// block they keep and cut into groups of NL = 256 / block: unit u = (bh, g) holds query blocks
+// qmap[u NL + L], L < NL (-1 past the last block).  Its tiles are the 64-key sub-tiles of the
+// union of its lists in ascending block order; ulist[u NK + i] = block << 4 | ownership bits
+// (bit L: list L keeps the block), ucount[u] = blocks * (block / 64) sub-tiles.  The unit's
+// tiles number max(1, ucount[u]): an empty unit gets one unowned tile, so that some workgroup
+// writes its output.  The grouping only decides which rows
+// share K/V tiles: any grouping gives the same result.
+
+constexpr int kPlanThreads = 256;
+constexpr int kMaxGroupNQ = 1024;   // heads with more query blocks keep the natural order
+
+// Grouping key of every query block: the smallest listed historical block, NK when the list has
+// none (the list is read as a set).  One wave per list.
+__global__ __launch_bounds__(kPlanThreads) void plan_keys_kernel(const int32_t* __restrict__ counts,
+                                                                 const int32_t* __restrict__ idx, int rows, int NK,
+                                                                 int h0, int h1, int32_t* __restrict__ keys) {
+  const int row = blockIdx.x * (kPlanThreads / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const int n = min(max(counts[row], 0), NK);
+  const int32_t* lst = idx + (size_t)row * NK;
+  int m = NK;
+  for (int a = lane; a < n; a += 64) {
+    const int j = lst[a];
+    if (j >= h0 && j < h1) m = min(m, j);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = min(m, __shfl_xor(m, off));
+  if (lane == 0) keys[row] = m;
+}
 
 __device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -300,26 +363,50 @@ __device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
   return base + incl - x;
 }
 
-constexpr int kPlanThreads = 256;
-
+// One workgroup per unit: its query blocks (rank by (key, block index) inside the head) and the
+// union of their lists with ownership bits.
 __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t* __restrict__ counts,
-                                                                  const int32_t* __restrict__ idx, int NQ, int NK,
+                                                                  const int32_t* __restrict__ idx,
+                                                                  const int32_t* __restrict__ keys, int NQ, int NK,
                                                                   int block, int row_tiles,
+                                                                  int32_t* __restrict__ qmap,
                                                                   int32_t* __restrict__ ulist,
                                                                   int32_t* __restrict__ ucount) {
   extern __shared__ __align__(16) uint32_t own[];     // 4 ownership bits per key block
   __shared__ int sh[kPlanThreads / 64];
+  __shared__ int qsel[4];
+  __shared__ int skey[kMaxGroupNQ];
   const int u = blockIdx.x;
-  const int bh = u / row_tiles, rt = u % row_tiles;
+  const int bh = u / row_tiles, g = u % row_tiles;
   const int tid = threadIdx.x;
+  const int NL = QR / block;
+  const int nsub = block / KT;
   const int nwords = (NK + 7) >> 3;
   for (int i = tid; i < nwords; i += kPlanThreads) own[i] = 0;
+  if (tid < 4) qsel[tid] = -1;
+  const bool grouped = NQ <= kMaxGroupNQ;
+  if (grouped)
+    for (int i = tid; i < NQ; i += kPlanThreads) skey[i] = keys[(size_t)bh * NQ + i];
   __syncthreads();
-  const int NL = QR / block;
-  const int q0 = rt * NL;
-  const int nlists = min(NL, NQ - q0);
-  for (int L = 0; L < nlists; ++L) {
-    const size_t row = (size_t)bh * NQ + q0 + L;
+  if (grouped) {
+    for (int i = tid; i < NQ; i += kPlanThreads) {
+      const int ki = skey[i];
+      int r = 0;
+      for (int j = 0; j < NQ; ++j) {
+        const int kj = skey[j];
+        r += (kj < ki) || (kj == ki && j < i);
+      }
+      if (r >= g * NL && r < g * NL + NL) qsel[r - g * NL] = i;
+    }
+  } else if (tid < NL && g * NL + tid < NQ) {
+    qsel[tid] = g * NL + tid;
+  }
+  __syncthreads();
+  if (tid < NL) qmap[(size_t)u * NL + tid] = qsel[tid];
+  for (int L = 0; L < NL; ++L) {
+    const int qb = qsel[L];
+    if (qb < 0) continue;
+    const size_t row = (size_t)bh * NQ + qb;
     const int n = min(max(counts[row], 0), NK);
     const int32_t* lst = idx + row * NK;
     for (int i = tid; i < n; i += kPlanThreads) {
@@ -347,88 +434,85 @@ __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t*
       if (bits) out[pos++] = ((8 * wi + e) << 4) | (int)bits;
     }
   }
-  if (tid == 0) ucount[u] = total;
+  if (tid == 0) ucount[u] = total * nsub;
 }
 
-// tstart[u] = tiles of units < u (each unit max(1, blocks * nsub) tiles); tstart[U] = total.
-__global__ __launch_bounds__(1024) void plan_scan_kernel(const int32_t* __restrict__ ucount, int U, int nsub,
-                                                         int64_t* __restrict__ tstart) {
-  __shared__ int64_t sh[16];
-  __shared__ int64_t carry;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) carry = 0;
-  __syncthreads();
-  for (int base = 0; base < U; base += 1024) {
-    const int u = base + tid;
-    const int64_t x = u < U ? (int64_t)max(1, ucount[u] * nsub) : 0;
-    int64_t incl = x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int64_t y = ((int64_t)__shfl_up((int)(incl >> 32), off) << 32) | (uint32_t)__shfl_up((int)incl, off);
-      if (lane >= off) incl += y;
-    }
-    if (lane == 63) sh[wave] = incl;
-    __syncthreads();
-    int64_t before = carry;
-    for (int wv = 0; wv < wave; ++wv) before += sh[wv];
-    if (u < U) tstart[u] = before + incl - x;
-    __syncthreads();
-    if (tid == 1023) carry = before + incl;
-    __syncthreads();
-  }
-  if (tid == 0) tstart[U] = carry;
-}
-
-// Expands every unit's union list into one record per 64-key tile at its place tstart[u] in the
-// global tile sequence (an empty unit gets one unowned record).
+// Expands unit u's union list into one record per 64-key tile at its place tstart[u] in the
+// global tile sequence, where tstart[u] = tiles of the units before u (summed here by the
+// workgroup); unit U-1 also writes tstart[U] = total.
 __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t* __restrict__ ulist,
-                                                                  const int32_t* __restrict__ ucount,
-                                                                  const int64_t* __restrict__ tstart, int NK,
-                                                                  int nsub, int block, int row_tiles,
-                                                                  int4* __restrict__ trec) {
+                                                                  const int32_t* __restrict__ ucount, int U, int NK,
+                                                                  int block, int row_tiles, int4* __restrict__ trec,
+                                                                  int32_t* __restrict__ tstart) {
+  __shared__ int sh[kPlanThreads / 64];
   const int u = blockIdx.x;
-  const int nb = ucount[u];
-  const int n = nb > 0 ? nb * nsub : 1;
-  const int bh = u / row_tiles, rt = u % row_tiles;
-  int4* out = trec + tstart[u];
-  for (int a = threadIdx.x; a < n; a += kPlanThreads) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  int part = 0;
+  for (int v = tid; v < u; v += kPlanThreads) part += max(1, ucount[v]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
+  if (lane == 0) sh[tid >> 6] = part;
+  __syncthreads();
+  int ts = 0;
+#pragma unroll
+  for (int wv = 0; wv < kPlanThreads / 64; ++wv) ts += sh[wv];
+  const int nt = ucount[u], n = nt > 0 ? nt : 1;
+  const int nsub = block / KT;
+  const int bh = u / row_tiles;
+  if (tid == 0) {
+    tstart[u] = ts;
+    if (u == U - 1) tstart[U] = ts + n;
+  }
+  int4* out = trec + ts;
+  const int32_t* ul = ulist + (size_t)u * NK;
+  for (int a = tid; a < n; a += kPlanThreads) {
     int key0 = 0, bits = 0;
-    if (nb > 0) {
-      const int e = ulist[(size_t)u * NK + (nsub == 2 ? (a >> 1) : a)];
+    if (nt > 0) {
+      const int e = ul[nsub == 2 ? (a >> 1) : a];
       key0 = (e >> 4) * block + (nsub == 2 ? (a & 1) * KT : 0);
       bits = e & 15;
     }
-    out[a] = int4{key0, bh, rt, bits | (a == 0 ? kFlFrom0 : 0) | (a == n - 1 ? kFlToEnd : 0)};
+    out[a] = int4{key0, bh, u, bits | (a == 0 ? kFlFrom0 : 0) | (a == n - 1 ? kFlToEnd : 0)};
   }
 }
 
-// Persistent workgroup lambda covers tiles [T lambda / P, T (lambda + 1) / P) of the global
-// tile sequence.
-__device__ inline int64_t range_begin(int64_t T, int lambda, int P) { return T * lambda / P; }
+// Stream lambda of P covers tiles [T lambda / P, T (lambda + 1) / P) of the global tile
+// sequence.
+__device__ inline int range_begin(int T, int lambda, int P) { return (int)((int64_t)T * lambda / P); }
 
-// Per-tile record written by the planner: x = first key, y = (batch, head), z = row tile of
-// the unit, w = ownership bits (0..3) | from0 << 4 | to_end << 5, where from0 / to_end mark the
-// unit's first / last tile.
-
-// One tile of a workgroup's range (wave-uniform).  fl adds to the record's bits: first / last
-// tile of a piece (the unit's tiles inside this range), valid (inside the range).
+// One tile of a workgroup's range (wave-uniform): record x = first key, y = (batch, head),
+// z = unit, w = ownership bits (0..3) | from0 | to_end (the unit's first / last tile), plus
+// first / last (the piece's, i.e. the unit's tiles inside this range) and valid.
 struct TileRef {
-  int key0, bh, rt, fl;
+  int key0, bh, unit, fl;
   __device__ bool valid() const { return fl & kFlValid; }
   __device__ bool owned(int list) const { return (fl >> list) & 1; }
 };
 
-__device__ inline TileRef fetch_tile(const int4* __restrict__ trec, int64_t t, int64_t t_begin, int64_t t_end) {
+__device__ inline TileRef make_tile(const int4& e, int t, int t_begin, int t_end) {
   TileRef r{0, 0, 0, 0};
   if (t < t_end) {
-    const int4 e = trec[t];
     r.key0 = e.x;
     r.bh = e.y;
-    r.rt = e.z;
+    r.unit = e.z;
     r.fl = e.w | kFlValid | ((e.w & kFlFrom0) || t == t_begin ? kFlFirst : 0) |
            ((e.w & kFlToEnd) || t + 1 == t_end ? kFlLast : 0);
   }
   return r;
+}
+
+// The record of tile t, read through the constant address space: the records are written by
+// an earlier kernel and never during this one, so the loads can go through the scalar cache
+// (s_load).  Index t is clamped into the range (t_end > t_begin); make_tile ignores a record
+// past the end.
+typedef __attribute__((address_space(4))) const int cint32;
+__device__ inline int4 load_tile(const int4* __restrict__ trec, int t, int t_end) {
+  const cint32* r = (const cint32*)(trec + (t < t_end ? t : t_end - 1));
+  return int4{r[0], r[1], r[2], r[3]};
+}
+
+__device__ inline TileRef fetch_tile(const int4* __restrict__ trec, int t, int t_begin, int t_end) {
+  return make_tile(load_tile(trec, t, t_end), t, t_begin, t_end);
 }
 
 // State of one wave's running unit piece.
@@ -439,7 +523,7 @@ struct WaveState {
   bf16x8 pb[4];
   bf16x8 qreg[D / 16];
   float m_run, l_run;
-  bool rows;        // the wave's rows exist (r0w < Lq)
+  bool rows;        // the wave's rows exist
   bool from0;       // the running piece starts at its unit's first tile
   int r0w;          // first query row of the wave in its (batch, head)
   int bh;
@@ -448,18 +532,17 @@ struct WaveState {
 // Shared arguments of the phases.
 struct KArgs {
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
   uint16_t* o;
   float* lse;
   float* part_o;
   float* part_m;
   float* part_l;
+  const int32_t* qmap;
   Geom gm;
-  int row_tiles;
   int lambda;
-  int my_list;
-  int r_off;
+  int my_list;      // list of the unit (query block) the wave's rows belong to
+  int r_sub;        // first row of the wave inside its query block
+  int r_off;        // first row of the wave inside the unit: my_list * block + r_sub
   int c32, h;
 };
 
@@ -470,7 +553,8 @@ __device__ __forceinline__ void start_piece(WaveState<D>& st, WaveCtx& w, const 
   constexpr int KS = D / 16, DT = D / 32;
   const Geom& gm = ka.gm;
   st.bh = t.bh;
-  st.r0w = t.rt * QR + ka.r_off;
+  const int qb = ka.qmap[(size_t)t.unit * (QR / gm.block) + ka.my_list];
+  st.r0w = qb >= 0 ? qb * gm.block + ka.r_sub : gm.Lq;
   st.rows = st.r0w < gm.Lq;
   st.from0 = t.fl & kFlFrom0;
   st.m_run = -INFINITY;
@@ -502,6 +586,7 @@ __device__ __forceinline__ void start_piece(WaveState<D>& st, WaveCtx& w, const 
 // Ends a piece: the normalised bf16 output (and lse) when the piece is the whole unit, else the
 // fp32 partial (O unnormalised, running max m, sum l) in slot 2 lambda (the range's first piece,
 // which continues an earlier range) or 2 lambda + 1 (its last, continued by a later range).
+// The stores are completed before returning (the tile-load waits count only tile loads).
 template <int D>
 __device__ __forceinline__ void end_piece(const WaveState<D>& st, bool to_end, const KArgs& ka) {
   constexpr int DT = D / 32;
@@ -510,8 +595,8 @@ __device__ __forceinline__ void end_piece(const WaveState<D>& st, bool to_end, c
   // lane holds O^T[32 dt + 8 (i/4) + 4 (l/32) + i%4][query r0w + l%32]
   const float l = st.l_run + __shfl_xor(st.l_run, 32);
   const int qrow = st.r0w + c32;
-  if (qrow >= gm.Lq) return;
-  if (st.from0 && to_end) {
+  if (qrow >= gm.Lq) {
+  } else if (st.from0 && to_end) {
     const float inv = l > 0.f ? 1.0f / l : 0.f;
     uint16_t* orow = ka.o + ((size_t)st.bh * gm.Lq + qrow) * D + 4 * h;
 #pragma unroll
@@ -540,85 +625,65 @@ __device__ __forceinline__ void end_piece(const WaveState<D>& st, bool to_end, c
       ka.part_l[prow] = l;
     }
   }
+  __builtin_amdgcn_s_waitcnt(0);
 }
 
-// M phase of tile `cur` (previous tile `prev`): P.V of prev, end of prev's piece, start of
-// cur's piece, Q.K^T of cur.
+// M phase of tile `cur` (flags prev_fl of the previous tile): P.V of the previous tile, end of
+// its piece, start of cur's piece, Q.K^T of cur.
 template <int D>
-__device__ __forceinline__ void m_phase(WaveState<D>& st, WaveCtx& w, const TileRef& prev, const TileRef& cur,
+__device__ __forceinline__ void m_phase(WaveState<D>& st, WaveCtx& w, int prev_fl, const TileRef& cur,
                                         const unsigned char* kcur, const unsigned char* vprev, const KArgs& ka) {
-  if (prev.valid()) {
-    if (prev.owned(ka.my_list) && st.rows) pv_tile<D>(vprev, st.pb, st.oacc, w.vbase);
-    if (prev.fl & kFlLast) end_piece<D>(st, prev.fl & kFlToEnd, ka);
-  }
-  if (cur.valid()) {
-    if (cur.fl & kFlFirst) start_piece<D>(st, w, cur, ka);
-    if (cur.owned(ka.my_list) && st.rows) qk_tile<D>(kcur, st.qreg, st.sacc, w.kbase);
-  }
+  if ((prev_fl & kFlValid) && ((prev_fl >> ka.my_list) & 1) && st.rows) pv_tile<D>(vprev, st.pb, st.oacc, w.vbase);
+  if ((prev_fl & kFlValid) && (prev_fl & kFlLast)) end_piece<D>(st, prev_fl & kFlToEnd, ka);
+  if (cur.valid() && (cur.fl & kFlFirst)) start_piece<D>(st, w, cur, ka);
+  if (cur.valid() && cur.owned(ka.my_list) && st.rows) qk_tile<D>(kcur, st.qreg, st.sacc, w.kbase);
 }
 
-// V phase of tile `cur`: masks, running max, rescale, P.
-template <int D>
-__device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, const TileRef& cur, const KArgs& ka) {
-  if (cur.valid() && cur.owned(ka.my_list) && st.rows) {
-    softmax_prep<D>(st.sacc, st.oacc, st.m_run, st.l_run, cur.key0, w);
-    softmax_p(st.sacc, st.pb, st.m_run, st.l_run, w.scale_log2);
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void issue_tile_loads(unsigned char* kdst, unsigned char* vdst, const TileRef& tk,
-                                                 const TileRef& tv, const KArgs& ka, const uint32_t* koff,
-                                                 const uint32_t* voff, int lw) {
-  using T = Tile<D>;
-  if (tk.valid()) {
-    const uint16_t* kh = ka.k + (size_t)tk.bh * ka.gm.Lk * D;
-    issue_rows<D, T::KINST, T::KPER>(kdst, kh, tk.key0, ka.gm.Lk, koff, lw);
-  }
-  if (tv.valid()) {
-    const uint16_t* vh = ka.v + (size_t)tv.bh * ka.gm.Lk * D;
-    issue_rows<D, T::VINST, T::VPER>(vdst, vh, tv.key0, ka.gm.Lk, voff, lw);
-  }
+// V phase of tile `cur`: masks, running max, rescale, P, with the tile loads `ld` spread in.
+template <int D, int NL>
+__device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, const TileRef& cur, const KArgs& ka,
+                                        const LoadSet<NL>& ld) {
+  const bool use = cur.valid() && cur.owned(ka.my_list) && st.rows;
+  if (use) softmax_prep<D>(st.sacc, st.oacc, st.m_run, st.l_run, cur.key0, w);
+  softmax_p<NL>(st.sacc, st.pb, st.m_run, st.l_run, w.scale_log2, use, ld);
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const int4* __restrict__ trec, const int64_t* __restrict__ tstart, uint16_t* __restrict__ o,
-    float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m, float* __restrict__ part_l,
-    Geom gm, int row_tiles, int U, float scale_log2) {
+    const int4* __restrict__ trec, const int32_t* __restrict__ tstart, const int32_t* __restrict__ qmap,
+    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
+    float* __restrict__ part_l, Geom gm, int U, float scale_log2) {
   using T = Tile<D>;
-  __shared__ __attribute__((aligned(1024))) unsigned char kbuf0[T::KBYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char kbuf1[T::KBYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char vbuf0[T::VBYTES];
-  __shared__ __attribute__((aligned(1024))) unsigned char vbuf1[T::VBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char kb0[T::KBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char kb1[T::KBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char vb0[T::VBYTES];
+  __shared__ __attribute__((aligned(1024))) unsigned char vb1[T::VBYTES];
 
   // XCD-aware range: hardware places consecutive workgroup ids on consecutive XCDs (round
   // robin over 8); the workgroups of one XCD get consecutive ranges, i.e. consecutive units
   // of the same heads, so each L2 keeps its heads' shared K/V.  P is a multiple of 8.
   const int P = gridDim.x;
   const int lambda = (blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3);
-  const int64_t Ttot = tstart[U];
-  const int64_t t_begin = range_begin(Ttot, lambda, P), t_end = range_begin(Ttot, lambda + 1, P);
+  const int Ttot = tstart[U];
+  const int t_begin = range_begin(Ttot, lambda, P), t_end = range_begin(Ttot, lambda + 1, P);
   if (t_begin >= t_end) return;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps tile-issue math scalar
-  const bool g1 = wave >= 4;                                    // the lagging group, which also loads
-  const int lw = wave & 3;
+  const bool g1 = wave >= 4;                                    // the lagging group
+  const int lw = wave & 3;                                      // wave within its group
   const int c32 = lane & 31, h = lane >> 5;
 
   KArgs ka;
   ka.q = q;
-  ka.k = k;
-  ka.v = v;
   ka.o = o;
   ka.lse = lse;
   ka.part_o = part_o;
   ka.part_m = part_m;
   ka.part_l = part_l;
+  ka.qmap = qmap;
   ka.gm = gm;
-  ka.row_tiles = row_tiles;
   ka.lambda = lambda;
   ka.c32 = c32;
   ka.h = h;
@@ -626,24 +691,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // or (128-row blocks) waves {0, 1, 4, 5} and {2, 3, 6, 7} own the two blocks
   if (gm.block == 64) {
     ka.my_list = wave & 3;
-    ka.r_off = (wave & 3) * 64 + (wave >> 2) * QW;
+    ka.r_sub = (wave >> 2) * QW;
+    ka.r_off = ka.my_list * 64 + ka.r_sub;
   } else {
     ka.my_list = (wave & 3) >> 1;
-    ka.r_off = ka.my_list * 128 + ((wave & 1) * 2 + (wave >> 2)) * QW;
+    ka.r_sub = ((wave & 1) * 2 + (wave >> 2)) * QW;
+    ka.r_off = ka.my_list * 128 + ka.r_sub;
   }
 
-  // lane-constant global offsets of this wave's tile loads (group 1 only)
-  uint32_t koff[T::KPER], voff[T::VPER];
+  // lane-constant global offsets of this wave's tile loads (group 1 loads K and V: KPER + 1 and
+  // VPER per wave, the last K load by wave 0 only)
+  uint32_t koff[T::KPER + 1], voff[T::VPER];
 #pragma unroll
-  for (int uu = 0; uu < T::KPER; ++uu) {
-    const int n = lw + 4 * uu;
-    koff[uu] = n < T::KINST ? slot_offset<D>(n, lane, T::KSLOTS) : 0x7fffffffu;
-  }
+  for (int j = 0; j <= T::KPER; ++j) koff[j] = slot_offset<D>(j < T::KPER ? lw + 4 * j : 4 * T::KPER, lane, T::KSLOTS);
 #pragma unroll
-  for (int uu = 0; uu < T::VPER; ++uu) {
-    const int n = lw + 4 * uu;
-    voff[uu] = n < T::VINST ? slot_offset<D>(n, lane, T::VSLOTS) : 0x7fffffffu;
-  }
+  for (int j = 0; j < T::VPER; ++j) voff[j] = slot_offset<D>(lw + 4 * j, lane, T::VSLOTS);
   WaveCtx w;
   w.key_lk = gm.Lk;
   w.kbase = c32 * T::KSTRIDE + 16 * h;
@@ -661,62 +723,91 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   st.r0w = 0;
   st.bh = 0;
 
-  const int64_t N = t_end - t_begin;
-  TileRef prev{0, 0, 0, 0};
+  const int N = t_end - t_begin;
+  int prev_fl = 0, prev_key0 = 0;      // the previous tile: flags and first key
   TileRef cur = fetch_tile(trec, t_begin, t_begin, t_end);
   TileRef nxt = fetch_tile(trec, t_begin + 1, t_begin, t_end);
 
+  // this (group 1) wave's loads of K(tile tk) into kdst and V(tile tv) into vdst
+  auto issue_loads = [&](unsigned char* kdst, const TileRef& tk, unsigned char* vdst, const TileRef& tv) {
+    const LoadSet<T::KPER> kl{tile_load<D>(kdst, k + (size_t)tk.bh * gm.Lk * D, tk.key0, gm.Lk, tk.valid()), lw, koff};
+    const LoadSet<T::VPER> vl{tile_load<D>(vdst, v + (size_t)tv.bh * gm.Lk * D, tv.key0, gm.Lk, tv.valid()), lw, voff};
+#pragma unroll
+    for (int j = 0; j < T::KPER; ++j) kl.issue(j);
+    if (lw == 0) kl.issue_at(4 * T::KPER, koff[T::KPER]);
+#pragma unroll
+    for (int j = 0; j < T::VPER; ++j) vl.issue(j);
+  };
   // prologue: K of the first tile
   if (g1) {
-    const TileRef none{0, 0, 0, 0};
-    issue_tile_loads<D>(kbuf0, vbuf0, cur, none, ka, koff, voff, lw);
+    const LoadSet<T::KPER> a{tile_load<D>(kb0, k + (size_t)cur.bh * gm.Lk * D, cur.key0, gm.Lk, cur.valid()), lw,
+                             koff};
+#pragma unroll
+    for (int j = 0; j < T::KPER; ++j) a.issue(j);
+    if (lw == 0) a.issue_at(4 * T::KPER, koff[T::KPER]);
     __builtin_amdgcn_s_waitcnt(0);
   }
   lds_barrier();
 
+  // Iteration h (phases A(h), B(h)); K(h) in kb[h & 1], V(h) in vb[h & 1].  Group 1 loads K(h+1)
+  // and V(h) in A(h) and waits for them at the end of B(h).  The record of tile h + 2 is fetched
+  // (scalar load) at the start of each V phase and decoded at its end, so that no scalar load is
+  // outstanding during an M phase (it would force the LDS operand reads there to wait for all
+  // LDS traffic).  Two iterations per trip, so that every buffer is a compile-time choice.
+  const LoadSet<0> none{TileLoad{}, 0, nullptr};
   auto run = [&](auto G1) {
     constexpr bool IS_G1 = decltype(G1)::value;
-    auto iteration = [&](unsigned char* kc, unsigned char* kn, unsigned char* vc, unsigned char* vp) {
+    TileRef nx2;
+    auto iteration = [&](int hh, unsigned char* kc, unsigned char* kn, unsigned char* vc, unsigned char* vp) {
       if constexpr (!IS_G1) {
-        m_phase<D>(st, w, prev, cur, kc, vp, ka);
+        m_phase<D>(st, w, prev_fl, cur, kc, vp, ka);
         lds_barrier();
-        v_phase<D>(st, w, cur, ka);
+        const int4 raw = load_tile(trec, t_begin + hh + 2, t_end);
+        v_phase<D, 0>(st, w, cur, ka, none);
+        nx2 = make_tile(raw, t_begin + hh + 2, t_begin, t_end);
         lds_barrier();
       } else {
-        v_phase<D>(st, w, prev, ka);
-        issue_tile_loads<D>(kn, vc, nxt, cur, ka, koff, voff, lw);
+        const int4 raw = load_tile(trec, t_begin + hh + 2, t_end);
+        v_phase<D, 0>(st, w, TileRef{prev_key0, 0, 0, prev_fl}, ka, none);
+        nx2 = make_tile(raw, t_begin + hh + 2, t_begin, t_end);
+        issue_loads(kn, nxt, vc, cur);
         barrier_keep_loads();
-        m_phase<D>(st, w, prev, cur, kc, vp, ka);
+        m_phase<D>(st, w, prev_fl, cur, kc, vp, ka);
         __builtin_amdgcn_s_waitcnt(0);
         lds_barrier();
       }
     };
-    for (int64_t hh = 0; hh <= N; hh += 2) {
-      iteration(kbuf0, kbuf1, vbuf0, vbuf1);
-      prev = cur;
+    auto advance = [&]() {
+      prev_fl = cur.fl;
+      prev_key0 = cur.key0;
       cur = nxt;
-      nxt = fetch_tile(trec, t_begin + hh + 2, t_begin, t_end);
+      nxt = nx2;
+    };
+    for (int hh = 0;; hh += 2) {
+      iteration(hh, kb0, kb1, vb0, vb1);
+      advance();
       if (hh + 1 > N) break;
-      iteration(kbuf1, kbuf0, vbuf1, vbuf0);
-      prev = cur;
-      cur = nxt;
-      nxt = fetch_tile(trec, t_begin + hh + 3, t_begin, t_end);
+      iteration(hh + 1, kb1, kb0, vb1, vb0);
+      advance();
+      if (hh + 2 > N) break;
     }
   };
   if (g1) run(std::true_type{});
   else run(std::false_type{});
-  // every load was waited for inside the loop (the last iterations issue none)
 }
 
-// Merges the pieces of units that were split across workgroups:
-// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s, over the pieces in workgroup order
-// (deterministic).  Thread t owns 4 columns and QR * D / (4 * kCombThreads) rows of the unit,
-// so the loads of all its rows are in flight together.
-constexpr int kCombThreads = 512;
+// Merges the pieces of units that were split across streams:
+// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s, over the pieces in stream order
+// (deterministic).  Workgroup (lambda, c) handles rows [32 c, 32 c + 32) of the unit that starts
+// inside stream lambda's range and continues past it, if there is one (each split unit has
+// exactly one such stream).
+constexpr int kCombRows = 32;
+constexpr int kCombThreads = 256;
 
 template <int D>
-__global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int64_t* __restrict__ tstart, int U, int P,
-                                                                    int row_tiles, int Lq,
+__global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_t* __restrict__ tstart,
+                                                                    const int32_t* __restrict__ qmap, int U, int P,
+                                                                    int row_tiles, int Lq, int block,
                                                                     const float* __restrict__ part_o,
                                                                     const float* __restrict__ part_m,
                                                                     const float* __restrict__ part_l,
@@ -724,18 +815,29 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int64_
                                                                     float* __restrict__ lse) {
   constexpr int CG = D / 4;                    // 4-column groups per row
   constexpr int RSTEP = kCombThreads / CG;     // rows per pass
-  constexpr int NI = QR / RSTEP;               // rows per thread
-  const int u = blockIdx.x;
-  const int64_t Ttot = tstart[U], ts = tstart[u], te = tstart[u + 1];
-  // workgroup (range) holding tile t: largest lambda with T lambda / P <= t
-  auto owner = [&](int64_t t) {
-    int64_t lam = ((t + 1) * P + Ttot - 1) / Ttot - 1;
+  constexpr int NI = kCombRows / RSTEP;        // rows per thread
+  const int lam0 = blockIdx.x;
+  const int Ttot = tstart[U];
+  const int b = range_begin(Ttot, lam0, P), e = range_begin(Ttot, lam0 + 1, P);
+  if (b >= e) return;
+  // unit holding tile e - 1: largest u with tstart[u] <= e - 1
+  int lo = 0, hi = U - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (tstart[mid] <= e - 1) lo = mid;
+    else hi = mid - 1;
+  }
+  const int u = lo;
+  const int ts = tstart[u], te = tstart[u + 1];
+  if (ts < b || te <= e) return;
+  // stream holding tile t: largest lambda with T lambda / P <= t
+  auto owner = [&](int t) {
+    const int64_t lam = ((int64_t)(t + 1) * P + Ttot - 1) / Ttot - 1;
     return (int)(lam < P - 1 ? lam : P - 1);
   };
-  const int la0 = owner(ts), la1 = owner(te - 1);
-  if (la0 == la1) return;                               // not split: written directly
-  const int bh = u / row_tiles, rt = u % row_tiles;
-  const int cg = threadIdx.x % CG, r0 = threadIdx.x / CG;
+  const int la1 = owner(te - 1);
+  const int bh = u / row_tiles;
+  const int cg = threadIdx.x % CG, r0 = blockIdx.y * kCombRows + threadIdx.x / CG;
   float m[NI], l[NI];
   f32x4 acc[NI];
 #pragma unroll
@@ -744,16 +846,16 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int64_
     l[i] = 0.f;
     acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // workgroups with an empty range (fewer tiles than workgroups) wrote no slot
-  for (int lam = la0; lam <= la1; ++lam) {
+  // streams with an empty range (fewer tiles than streams) wrote no slot
+  for (int lam = lam0; lam <= la1; ++lam) {
     if (range_begin(Ttot, lam, P) == range_begin(Ttot, lam + 1, P)) continue;
-    const int slot = lam == la0 ? 2 * lam + 1 : 2 * lam;
+    const int slot = lam == lam0 ? 2 * lam + 1 : 2 * lam;
 #pragma unroll
     for (int i = 0; i < NI; ++i) m[i] = fmaxf(m[i], part_m[(size_t)slot * QR + r0 + RSTEP * i]);
   }
-  for (int lam = la0; lam <= la1; ++lam) {
+  for (int lam = lam0; lam <= la1; ++lam) {
     if (range_begin(Ttot, lam, P) == range_begin(Ttot, lam + 1, P)) continue;
-    const int slot = lam == la0 ? 2 * lam + 1 : 2 * lam;
+    const int slot = lam == lam0 ? 2 * lam + 1 : 2 * lam;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const size_t pr = (size_t)slot * QR + r0 + RSTEP * i;
@@ -765,8 +867,10 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int64_
   }
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
-    const int qrow = rt * QR + r0 + RSTEP * i;
-    if (qrow < Lq) {
+    const int r = r0 + RSTEP * i;                       // row inside the unit
+    const int qb = qmap[(size_t)u * (QR / block) + r / block];
+    const int qrow = qb * block + r % block;
+    if (qb >= 0 && qrow < Lq) {
       const float inv = l[i] > 0.f ? 1.0f / l[i] : 0.f;
       u32x2 ow;
       ow[0] = pack_bf16x2(acc[i][0] * inv, acc[i][1] * inv);
@@ -780,9 +884,11 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int64_
 
 struct AttnWs {
   int4* trec;
+  int32_t* qmap;
+  int32_t* keys;
   int32_t* ulist;
   int32_t* ucount;
-  int64_t* tstart;
+  int32_t* tstart;
   float* part_o;
   float* part_m;
   float* part_l;
@@ -799,12 +905,16 @@ AttnWs attn_ws_layout(const Dims& dm, void* base) {
   // at most max(1, NK * nsub) tiles per unit
   w.trec = (int4*)(b + off);
   off += align256(U * (size_t)dm.NK * (dm.block / KT) * sizeof(int4));
+  w.qmap = (int32_t*)(b + off);
+  off += align256(U * (size_t)(QR / dm.block) * sizeof(int32_t));
+  w.keys = (int32_t*)(b + off);
+  off += align256((size_t)dm.BH * dm.NQ * sizeof(int32_t));
   w.ulist = (int32_t*)(b + off);
-  off += align256(U * dm.NK * sizeof(int32_t));
+  off += align256(U * (size_t)dm.NK * sizeof(int32_t));
   w.ucount = (int32_t*)(b + off);
   off += align256(U * sizeof(int32_t));
-  w.tstart = (int64_t*)(b + off);
-  off += align256((U + 1) * sizeof(int64_t));
+  w.tstart = (int32_t*)(b + off);
+  off += align256((U + 1) * sizeof(int32_t));
   w.part_o = (float*)(b + off);
   off += align256(slots * QR * dm.d * sizeof(float));
   w.part_m = (float*)(b + off);
@@ -834,30 +944,32 @@ hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void*
                        const int32_t* idx, float scale, void* o, float* lse, void* ws, hipStream_t st) {
   const int row_tiles = ceil_div(dm.Lq, QR);
   const int U = dm.BH * row_tiles;
-  const int nsub = dm.block / KT;
   const int P = persistent_workgroups();
   AttnWs w = attn_ws_layout(dm, ws);
   Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
   const float scale_log2 = scale * 1.4426950408889634f;
+  const int rows = dm.BH * dm.NQ;
+  hipLaunchKernelGGL(plan_keys_kernel, dim3(ceil_div(rows, kPlanThreads / 64)), dim3(kPlanThreads), 0, st, counts,
+                     idx, rows, dm.NK, dm.h0, dm.h1, w.keys);
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
-                     st, counts, idx, dm.NQ, dm.NK, dm.block, row_tiles, w.ulist, w.ucount);
-  hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(1024), 0, st, w.ucount, U, nsub, w.tstart);
-  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, w.tstart, dm.NK, nsub,
-                     dm.block, row_tiles, w.trec);
+                     st, counts, idx, w.keys, dm.NQ, dm.NK, dm.block, row_tiles, w.qmap, w.ulist, w.ucount);
+  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, U, dm.NK, dm.block,
+                     row_tiles, w.trec, w.tstart);
   if (dm.d == 128)
     hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, (uint16_t*)o, lse,
-                       w.part_o, w.part_m, w.part_l, gm, row_tiles, U, scale_log2);
+                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, w.qmap, (uint16_t*)o, lse,
+                       w.part_o, w.part_m, w.part_l, gm, U, scale_log2);
   else
     hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, (uint16_t*)o, lse,
-                       w.part_o, w.part_m, w.part_l, gm, row_tiles, U, scale_log2);
+                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, w.qmap, (uint16_t*)o, lse,
+                       w.part_o, w.part_m, w.part_l, gm, U, scale_log2);
+  const dim3 cgrid(P, QR / kCombRows);
   if (dm.d == 128)
-    hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(U), dim3(kCombThreads), 0, st, w.tstart, U, P, row_tiles,
-                       dm.Lq, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
+    hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.qmap, U, P, row_tiles,
+                       dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(U), dim3(kCombThreads), 0, st, w.tstart, U, P, row_tiles,
-                       dm.Lq, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
+    hipLaunchKernelGGL(attn_combine_kernel<64>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.qmap, U, P, row_tiles,
+                       dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   return hipGetLastError();
 }
 
