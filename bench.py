@@ -2,14 +2,16 @@
 """Benchmark of the AR block-sparse attention hot path on one MI355X.
 
 A step is one pass of the whole path over one synthetic batch already resident in HBM:
-la_select_blocks (pool Q, pool+score historical K, select and compact) followed by
-la_sparse_attn_fwd over the kept blocks.  Prints ONE JSON line.
+la_select_blocks (pool Q, pool+score historical K, select and compact) followed by the three
+steps of la_sparse_attn_fwd over the kept blocks (plan, run, merge), each called through its own
+entry point so that HIP events on the launch stream time every stage.  Prints ONE JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
 value = kept-block TFLOP/s of the whole step (kept FLOPs / step time).  The line also
 carries the per-kernel split, the dense baseline (same attention kernel, every block
-kept), the roofline of the attention kernel and the fp64 oracle's CPU rate.
+kept), the roofline of the attention kernel (la_sparse_attn_run launches exactly that one
+kernel, so its event time is the kernel's launch duration) and the fp64 oracle's CPU rate.
 """
 from __future__ import annotations
 
@@ -67,8 +69,9 @@ def traffic_from_profile(kernel_tag: str, workload: str, digest: str, launches_b
 
 
 def cpu_baseline(wl, inp, mask_np, target_s: float):
-    """The fp64 oracle on the host: selection of one head plus attention of as many of its
-    query blocks as fit in about target_s seconds; rate in kept TFLOP/s."""
+    """The fp64 oracle on the host, head after head (selection of the head, then fp64 attention of
+    its query blocks on the GPU's mask) until about target_s seconds have passed; rate in kept
+    TFLOP/s over the heads done."""
     from oracle import la_oracle as O
     threads = None
     try:
@@ -77,32 +80,38 @@ def cpu_baseline(wl, inp, mask_np, target_s: float):
         threads = max((i.get("num_threads", 1) for i in info), default=1)
     except Exception:
         pass
-    t0 = time.perf_counter()
-    sel = O.select_blocks(inp["q"][:, :1], inp["k"][:, :1], wl.block, tau=wl.tau)
-    t_sel = time.perf_counter() - t0
+    F = wl.frame_tokens if wl.causal_frames else 0
     flops = 0
-    rows_done = 0
-    t1 = time.perf_counter()
-    i = 0
-    while i < wl.nq:
-        chunk = list(range(i, min(i + 8, wl.nq)))
-        O.attention_rows(inp["q"], inp["k"], inp["v"], mask_np, wl.block, [(0, 0, r) for r in chunk],
-                         frame_tokens=wl.frame_tokens if wl.causal_frames else 0)
-        for r in chunk:
-            lo, hi = r * wl.block, min((r + 1) * wl.block, wl.Lq)
-            nk = sum(min((m + 1) * wl.block, wl.Lk) - m * wl.block for m in np.nonzero(mask_np[0, 0, r])[0])
-            flops += 4 * wl.d * (hi - lo) * nk
-        rows_done += len(chunk)
-        i += len(chunk)
-        if time.perf_counter() - t1 > target_s:
+    blocks = 0
+    t0 = time.perf_counter()
+    heads = 0
+    passes = 0
+    while True:      # whole passes over the heads until about target_s of work is done
+        for b in range(wl.B):
+            for h in range(wl.H):
+                O.select_blocks(inp["q"][b:b + 1, h:h + 1], inp["k"][b:b + 1, h:h + 1], wl.block, tau=wl.tau,
+                                n_text=wl.n_text)
+                for i0 in range(0, wl.nq, 8):
+                    rows = [(b, h, r) for r in range(i0, min(i0 + 8, wl.nq))]
+                    O.attention_rows(inp["q"], inp["k"], inp["v"], mask_np, wl.block, rows, frame_tokens=F)
+                    for _, _, r in rows:
+                        lo, hi = r * wl.block, min((r + 1) * wl.block, wl.Lq)
+                        nk = sum(min((m + 1) * wl.block, wl.Lk) - m * wl.block for m in np.nonzero(mask_np[b, h, r])[0])
+                        flops += 4 * wl.d * (hi - lo) * nk
+                    blocks += len(rows)
+                heads += 1
+                if time.perf_counter() - t0 > target_s:
+                    break
+            if time.perf_counter() - t0 > target_s:
+                break
+        passes += 1
+        if time.perf_counter() - t0 > target_s:
             break
-    t_attn = time.perf_counter() - t1
-    # selection share of one query block of this head, added pro rata
-    t_total = t_attn + t_sel * rows_done / wl.nq
-    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": threads or os.cpu_count(),
+    t_total = time.perf_counter() - t0
+    return {"value": round(flops / t_total / 1e12, 5), "unit": "TFLOP/s", "cores": threads or os.cpu_count(),
             "kind": "oracle",
-            "sample": f"head 0 of {wl.name}: selection over its {wl.nq} query blocks (pro rata) + fp64 attention of "
-                      f"{rows_done}/{wl.nq} query blocks on the GPU's mask; {flops / 1e9:.1f} GFLOP kept in "
+            "sample": f"{heads} heads ({passes} pass(es) over the {wl.B * wl.H} heads) of {wl.name}: fp64 selection of each head and fp64 attention of "
+                      f"its {blocks // max(heads, 1)} query blocks on the GPU's mask; {flops / 1e9:.1f} GFLOP kept in "
                       f"{t_total:.1f} s; os.cpu_count()={os.cpu_count()}, "
                       f"affinity={len(os.sched_getaffinity(0))}"}
 
@@ -134,13 +143,11 @@ def main():
     idx = torch.empty((B, H, NQ, NK), dtype=torch.int32, device=dev)
     o = torch.empty_like(g["q"])
     stream = torch.cuda.current_stream(dev)
-
-    def select():
-        la.select_blocks(g["q"], g["k"], wl.block, wl.tau, n_text=wl.n_text, ws=ws, out=(mask, counts, idx))
-
-    def attn(cnt, ix):
-        la.sparse_attn_fwd(g["q"], g["k"], g["v"], cnt, ix, wl.block, n_text=wl.n_text, frame_tokens=F,
-                           ws=ws, out=o)
+    # the calls with their arguments marshalled once, so that the host stays ahead of the GPU
+    select = la.bind_select(g["q"], g["k"], wl.block, wl.tau, mask, counts, idx, ws, n_text=wl.n_text)
+    plan, run, merge = la.bind_attn_steps(g["q"], g["k"], g["v"], counts, idx, wl.block, o, ws, n_text=wl.n_text,
+                                          frame_tokens=F)
+    stages = (select, plan, run, merge)
 
     if args.calibrate_copy:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
@@ -150,24 +157,24 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     for _ in range(args.warmup):
-        select()
-        attn(counts, idx)
+        for f in stages:
+            f()
     torch.cuda.synchronize()
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for it in range(K):
         ev[it][0].record(stream)
-        select()
-        ev[it][1].record(stream)
-        attn(counts, idx)
-        ev[it][2].record(stream)
+        for j, f in enumerate(stages):
+            f()
+            ev[it][j + 1].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / K
-    t_sel = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(K)])
-    t_att = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(K)])
+    st_ms = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(len(stages))] for i in range(K)])
+    t_sel, t_plan, t_run, t_merge = (st_ms[:, j] for j in range(4))
+    t_att = t_plan + t_run + t_merge
 
     mask_np = mask.cpu().numpy()
     nq_valid = np.array([min((i + 1) * wl.block, Lq) - i * wl.block for i in range(NQ)], np.int64)
@@ -177,28 +184,33 @@ def main():
     dense_flops = 4.0 * B * H * Lq * wl.Lk * d
     rho = kept_flops / dense_flops
 
-    # dense baseline: the same attention kernel over every key block
+    # dense baseline: the same attention steps over every key block
     dense_ms = None
     if not args.no_dense and not args.profile_only:
         dmask = torch.ones_like(mask)
         dcounts, didx = la.mask_to_list(dmask, wl.block, Lq, wl.Lk, d)
-        for _ in range(3):
-            attn(dcounts, didx)
+        dsteps = la.bind_attn_steps(g["q"], g["k"], g["v"], dcounts, didx, wl.block, o, ws, n_text=wl.n_text,
+                                    frame_tokens=F)
+        for _ in range(2):
+            for f in dsteps:
+                f()
         torch.cuda.synchronize()
-        nd = max(3, min(K, 20))
-        evd = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(nd)]
-        for it in range(nd):
-            evd[it][0].record(stream)
-            attn(dcounts, didx)
-            evd[it][1].record(stream)
+        nd = max(3, min(K, 10))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(nd):
+            for f in dsteps:
+                f()
+        e1.record(stream)
         torch.cuda.synchronize()
-        dense_ms = float(np.median([evd[i][0].elapsed_time(evd[i][1]) for i in range(nd)]))
-        del dmask, dcounts, didx
+        dense_ms = e0.elapsed_time(e1) / nd
+        del dmask, dcounts, didx, dsteps
 
     sel_ms = float(np.mean(t_sel))
     att_ms = float(np.mean(t_att))
+    run_ms = float(np.mean(t_run))
     value = kept_flops / (ms_step * 1e-3) / 1e12
-    achieved = kept_flops / (att_ms * 1e-3) / 1e12
+    achieved = kept_flops / (run_ms * 1e-3) / 1e12
     hbm_sel_bytes = 2.0 * B * H * (Lq + (wl.Lk - Lq - wl.n_text)) * d + mask_np.size * (1 + 4) + counts.numel() * 4
     digest = src_digest("attn.hip")
     traffic = traffic_from_profile("attn_fwd", wl.name, digest, kept_flops)
@@ -221,10 +233,14 @@ def main():
         "select_ms": round(sel_ms, 4),
         "attn_ms": round(att_ms, 4),
         "attn_ms_p10_p90": [round(float(np.percentile(t_att, 10)), 4), round(float(np.percentile(t_att, 90)), 4)],
+        "attn_plan_ms": round(float(np.mean(t_plan)), 4),
+        "attn_run_ms": round(run_ms, 4),
+        "attn_merge_ms": round(float(np.mean(t_merge)), 4),
         "keep_ratio": round(rho, 5),
         "kept_tflop": round(kept_flops / 1e12, 5),
-        "attn_tflops": round(achieved, 2),
-        "attn_pct_mfma_peak": round(100 * achieved / MFMA_BF16_PEAK_TFLOPS, 2),
+        "attn_tflops": round(kept_flops / (att_ms * 1e-3) / 1e12, 2),
+        "attn_run_tflops": round(achieved, 2),
+        "attn_run_pct_mfma_peak": round(100 * achieved / MFMA_BF16_PEAK_TFLOPS, 2),
         "select_gbs": round(hbm_sel_bytes / (sel_ms * 1e-3) / 1e9, 1),
         "dense_attn_ms": None if dense_ms is None else round(dense_ms, 4),
         "dense_tflops": None if dense_ms is None else round(dense_flops / (dense_ms * 1e-3) / 1e12, 2),
@@ -232,7 +248,7 @@ def main():
         "ideal_speedup": round(1.0 / rho, 3),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": traffic, "kernel": "attn_fwd_kernel<128>", "src_digest": digest},
+                     "traffic": traffic, "kernel": f"attn_fwd_kernel<{d}>", "src_digest": digest},
         "gpu": torch.cuda.get_device_name(dev),
         "gen_s": round(t_gen, 2),
     }

@@ -61,7 +61,7 @@ typedef enum la_status {
  *   frame_tokens  0: every kept key is visible to every query.  F > 0: frame-causal
  *               inside the chunk, query token t (chunk position) sees chunk key
  *               n (n >= Lk - Lq) only if (n - (Lk - Lq)) / F <= t / F; context keys
- *               stay visible.  Used by la_sparse_attn_fwd only.
+ *               stay visible.  Used by the attention calls only.
  * Key block m is forced (always kept, never scored) when it overlaps the text
  * tokens [0, n_text) or the chunk [Lk - Lq, Lk); the others are the M historical
  * candidates, block indices [ceil(n_text/block), floor((Lk-Lq)/block)).
@@ -74,10 +74,11 @@ typedef struct la_shape {
   int32_t frame_tokens;
 } la_shape;
 
-/* Bytes of scratch space la_select_blocks, la_select_blocks_topk and
- * la_sparse_attn_fwd need for this shape (the maximum over the three; the
- * attention pass keeps its work plan and the partial results of work split
- * across workgroups there).  Returns 0 for an invalid shape. */
+/* Bytes of scratch space the selection and attention calls need for this shape
+ * (the maximum over them; the attention pass keeps its work plan and the partial
+ * results of work split across workgroups there).  One ws may serve all calls in
+ * stream order; a selection call overwrites an attention plan held in the same ws.
+ * Returns 0 for an invalid shape. */
 size_t la_workspace_bytes(const la_shape* shape);
 
 /* Cumulative-mass block selection.
@@ -119,6 +120,30 @@ la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void
 la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k, const void* v,
                              const int32_t* counts, const int32_t* idx, float scale,
                              void* o, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* la_sparse_attn_fwd in its three steps, for callers that time or reuse them.
+ * The work plan depends only on the lists: units of 256 query rows (query blocks of a
+ * head grouped by the first historical block they keep), the union of their lists as
+ * 64-key tiles, and the split of all tiles into equal ranges over one persistent
+ * workgroup per CU.  It lives in ws.
+ *
+ * la_sparse_attn_plan: builds the plan for `shape` from counts/idx (read as in
+ *   la_sparse_attn_fwd) into ws.
+ * la_sparse_attn_run: the attention pass over the plan in ws (built by
+ *   la_sparse_attn_plan for the same shape; it may be run for several q, k, v that
+ *   share the lists).  Writes o and lse for the query rows of units processed whole by
+ *   one workgroup, and partial results (O, running max, sum) into ws for the others.
+ * la_sparse_attn_merge: merges those partials into o and lse (the buffers given to the
+ *   run; lse may be NULL if it was NULL there).
+ * Plan, run and merge must follow each other on one stream with the same ws.
+ * Arguments, alignment and errors as for la_sparse_attn_fwd. */
+la_status la_sparse_attn_plan(const la_shape* shape, const int32_t* counts, const int32_t* idx,
+                              void* ws, size_t ws_bytes, void* stream);
+la_status la_sparse_attn_run(const la_shape* shape, const void* q, const void* k, const void* v,
+                             float scale, void* o, float* lse, void* ws, size_t ws_bytes,
+                             void* stream);
+la_status la_sparse_attn_merge(const la_shape* shape, void* o, float* lse, void* ws,
+                               size_t ws_bytes, void* stream);
 
 /* Compacts a block mask (uint8 [B, H, NQ, NK], non-zero = kept) into the
  * counts/idx form la_sparse_attn_fwd reads.  Needs no workspace. */

@@ -84,19 +84,66 @@ la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void
   return select_common(shape, q, k, 1.0f, keep_blocks, mask, counts, idx, ws, ws_bytes, stream);
 }
 
+static la_status attn_check(const la_shape* shape, Dims* dm, void* ws, size_t ws_bytes) {
+  la_status st = make_dims(shape, dm);
+  if (st != LA_OK) return st;
+  if (!ws || ws_bytes < attn_ws_bytes(*dm) || ((uintptr_t)ws & 255u)) return LA_ERR_WORKSPACE;
+  return LA_OK;
+}
+
+static la_status qkvo_check(const void* q, const void* k, const void* v, void* o, float scale) {
+  if (!q || !k || !v || !o) return LA_ERR_ARG;
+  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return LA_ERR_ARG;
+  if (isnan(scale) || isinf(scale)) return LA_ERR_ARG;
+  return LA_OK;
+}
+
+static float effective_scale(float scale, const Dims& dm) {
+  return scale > 0.0f ? scale : 1.0f / sqrtf((float)dm.d);
+}
+
 la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k, const void* v,
                              const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
                              void* ws, size_t ws_bytes, void* stream) {
   Dims dm;
-  la_status st = make_dims(shape, &dm);
+  la_status st = attn_check(shape, &dm, ws, ws_bytes);
+  if (st == LA_OK) st = qkvo_check(q, k, v, o, scale);
+  if (st == LA_OK && (!counts || !idx)) st = LA_ERR_ARG;
   if (st != LA_OK) return st;
-  if (!q || !k || !v || !counts || !idx || !o) return LA_ERR_ARG;
-  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o)) return LA_ERR_ARG;
-  if (isnan(scale) || isinf(scale)) return LA_ERR_ARG;
-  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)dm.d);
-  size_t need = attn_ws_bytes(dm);
-  if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return LA_ERR_WORKSPACE;
-  hipError_t e = launch_attn(dm, q, k, v, counts, idx, scale, o, lse, ws, (hipStream_t)stream);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = launch_attn_plan(dm, counts, idx, ws, s);
+  if (e == hipSuccess) e = launch_attn_run(dm, q, k, v, effective_scale(scale, dm), o, lse, ws, s);
+  if (e == hipSuccess) e = launch_attn_merge(dm, o, lse, ws, s);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_sparse_attn_plan(const la_shape* shape, const int32_t* counts, const int32_t* idx, void* ws,
+                              size_t ws_bytes, void* stream) {
+  Dims dm;
+  la_status st = attn_check(shape, &dm, ws, ws_bytes);
+  if (st != LA_OK) return st;
+  if (!counts || !idx) return LA_ERR_ARG;
+  hipError_t e = launch_attn_plan(dm, counts, idx, ws, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_sparse_attn_run(const la_shape* shape, const void* q, const void* k, const void* v, float scale,
+                             void* o, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  Dims dm;
+  la_status st = attn_check(shape, &dm, ws, ws_bytes);
+  if (st == LA_OK) st = qkvo_check(q, k, v, o, scale);
+  if (st != LA_OK) return st;
+  hipError_t e = launch_attn_run(dm, q, k, v, effective_scale(scale, dm), o, lse, ws, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_sparse_attn_merge(const la_shape* shape, void* o, float* lse, void* ws, size_t ws_bytes,
+                               void* stream) {
+  Dims dm;
+  la_status st = attn_check(shape, &dm, ws, ws_bytes);
+  if (st != LA_OK) return st;
+  if (!o || misaligned(o)) return LA_ERR_ARG;
+  hipError_t e = launch_attn_merge(dm, o, lse, ws, (hipStream_t)stream);
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 

@@ -940,14 +940,10 @@ int persistent_workgroups() {
 
 size_t attn_ws_bytes(const Dims& dm) { return attn_ws_layout(dm, nullptr).bytes; }
 
-hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void* v, const int32_t* counts,
-                       const int32_t* idx, float scale, void* o, float* lse, void* ws, hipStream_t st) {
+hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t* idx, void* ws, hipStream_t st) {
   const int row_tiles = ceil_div(dm.Lq, QR);
   const int U = dm.BH * row_tiles;
-  const int P = persistent_workgroups();
   AttnWs w = attn_ws_layout(dm, ws);
-  Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
-  const float scale_log2 = scale * 1.4426950408889634f;
   const int rows = dm.BH * dm.NQ;
   hipLaunchKernelGGL(plan_keys_kernel, dim3(ceil_div(rows, kPlanThreads / 64)), dim3(kPlanThreads), 0, st, counts,
                      idx, rows, dm.NK, dm.h0, dm.h1, w.keys);
@@ -955,6 +951,17 @@ hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void*
                      st, counts, idx, w.keys, dm.NQ, dm.NK, dm.block, row_tiles, w.qmap, w.ulist, w.ucount);
   hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, U, dm.NK, dm.block,
                      row_tiles, w.trec, w.tstart);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_run(const Dims& dm, const void* q, const void* k, const void* v, float scale, void* o,
+                           float* lse, void* ws, hipStream_t st) {
+  const int row_tiles = ceil_div(dm.Lq, QR);
+  const int U = dm.BH * row_tiles;
+  const int P = persistent_workgroups();
+  AttnWs w = attn_ws_layout(dm, ws);
+  Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
+  const float scale_log2 = scale * 1.4426950408889634f;
   if (dm.d == 128)
     hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
                        (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, w.qmap, (uint16_t*)o, lse,
@@ -963,6 +970,14 @@ hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void*
     hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
                        (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, w.qmap, (uint16_t*)o, lse,
                        w.part_o, w.part_m, w.part_l, gm, U, scale_log2);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipStream_t st) {
+  const int row_tiles = ceil_div(dm.Lq, QR);
+  const int U = dm.BH * row_tiles;
+  const int P = persistent_workgroups();
+  AttnWs w = attn_ws_layout(dm, ws);
   const dim3 cgrid(P, QR / kCombRows);
   if (dm.d == 128)
     hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.qmap, U, P, row_tiles,

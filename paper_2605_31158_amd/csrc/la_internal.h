@@ -32,8 +32,8 @@ la_status make_dims(const la_shape* s, Dims* out);
 
 // Workspace layout of the selection pass: pooled queries then the score matrix.
 size_t select_ws_bytes(const Dims& dm);
-// Workspace of the attention pass: work plan (union lists, tile prefix sums) and the partial
-// (O, m, l) slots of units split across persistent workgroups.
+// Workspace of the attention pass: work plan (grouping, union lists, tile records, tile prefix
+// sums) and the partial (O, m, l) slots of units split across persistent workgroups.
 size_t attn_ws_bytes(const Dims& dm);
 
 // Launchers (defined next to their kernels); they only enqueue.
@@ -41,9 +41,12 @@ hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau
                          uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st);
 hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,
                                hipStream_t st);
-hipError_t launch_attn(const Dims& dm, const void* q, const void* k, const void* v,
-                       const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
-                       void* ws, hipStream_t st);
+// The attention pass: work plan from the lists, the attention kernel over the plan, merge of
+// the units split across workgroups.
+hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t* idx, void* ws, hipStream_t st);
+hipError_t launch_attn_run(const Dims& dm, const void* q, const void* k, const void* v, float scale, void* o,
+                           float* lse, void* ws, hipStream_t st);
+hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipStream_t st);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

@@ -43,6 +43,9 @@ _SIGNATURES = {
     "la_select_blocks": (ctypes.c_int, [_SP, _P, _P, ctypes.c_float, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_select_blocks_topk": (ctypes.c_int, [_SP, _P, _P, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_fwd": (ctypes.c_int, [_SP, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_sparse_attn_plan": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_sparse_attn_run": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_sparse_attn_merge": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_mask_to_list": (ctypes.c_int, [_SP, _P, _P, _P, _P]),
     "la_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "la_abi_version": (ctypes.c_int32, []),
@@ -174,6 +177,57 @@ def sparse_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, counts: t
           ctypes.c_float(scale if scale is not None else 0.0), _ptr(o), _ptr(lse), _ptr(ws),
           ctypes.c_size_t(nbytes), _stream(q))
     return (o, lse) if (want_lse or lse_out is not None) else o
+
+
+class BoundCall:
+    """One C-ABI call with its arguments marshalled once (tensors, shape, stream fixed), for
+    loops that issue the same call many times; calling it returns nothing and raises LaError
+    on a failed status."""
+
+    def __init__(self, fn: str, *args, keep=()):
+        self._name = fn
+        self._fn = getattr(lib(), fn)
+        self._args = args
+        self._keep = keep          # tensors and structs the raw pointers refer to
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != LA_OK:
+            raise LaError(self._name, st)
+
+
+def bind_attn_steps(q, k, v, counts, idx, block, o, ws, scale: Optional[float] = None, n_text: int = 0,
+                    frame_tokens: int = 0, lse: Optional[torch.Tensor] = None):
+    """(plan, run, merge) of la_sparse_attn_fwd as BoundCalls on fixed tensors and the current
+    stream; plan + run + merge computes the same o (and lse) as sparse_attn_fwd."""
+    _check_qkv("q", q)
+    B, H, Lq, d = q.shape
+    _check_qkv("k", k, B, H, d)
+    _check_qkv("v", v, B, H, d)
+    Lk = k.shape[2]
+    shape = make_shape(B, H, Lq, Lk, d, block, n_text, frame_tokens)
+    nbytes = ctypes.c_size_t(ws.numel())
+    st = _stream(q)
+    keep = (q, k, v, counts, idx, o, ws, lse, shape)
+    sc = ctypes.c_float(scale if scale is not None else 0.0)
+    plan = BoundCall("la_sparse_attn_plan", ctypes.byref(shape), _ptr(counts), _ptr(idx), _ptr(ws), nbytes, st,
+                     keep=keep)
+    run = BoundCall("la_sparse_attn_run", ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), sc, _ptr(o), _ptr(lse),
+                    _ptr(ws), nbytes, st, keep=keep)
+    merge = BoundCall("la_sparse_attn_merge", ctypes.byref(shape), _ptr(o), _ptr(lse), _ptr(ws), nbytes, st,
+                      keep=keep)
+    return plan, run, merge
+
+
+def bind_select(q, k, block, tau, mask, counts, idx, ws, n_text: int = 0) -> BoundCall:
+    """la_select_blocks as a BoundCall on fixed tensors and the current stream."""
+    _check_qkv("q", q)
+    B, H, Lq, d = q.shape
+    _check_qkv("k", k, B, H, d)
+    shape = make_shape(B, H, Lq, k.shape[2], d, block, n_text, 0)
+    return BoundCall("la_select_blocks", ctypes.byref(shape), _ptr(q), _ptr(k), ctypes.c_float(tau), _ptr(mask),
+                     _ptr(counts), _ptr(idx), _ptr(ws), ctypes.c_size_t(ws.numel()), _stream(q),
+                     keep=(q, k, mask, counts, idx, ws, shape))
 
 
 def mask_to_list(mask: torch.Tensor, block: int, Lq: int, Lk: int, d: int = 128):

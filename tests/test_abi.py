@@ -72,6 +72,19 @@ def test_bad_shapes_rejected(bad):
     assert lib.la_sparse_attn_fwd(ctypes.byref(s), p, p, p, p, p, ctypes.c_float(0), p, None, p, 1 << 30,
                                   None) == la.LA_ERR_SHAPE
     assert lib.la_mask_to_list(ctypes.byref(s), p, p, p, None) == la.LA_ERR_SHAPE
+    assert lib.la_sparse_attn_plan(ctypes.byref(s), p, p, p, 1 << 30, None) == la.LA_ERR_SHAPE
+    assert lib.la_sparse_attn_run(ctypes.byref(s), p, p, p, ctypes.c_float(0), p, None, p, 1 << 30,
+                                  None) == la.LA_ERR_SHAPE
+    assert lib.la_sparse_attn_merge(ctypes.byref(s), p, None, p, 1 << 30, None) == la.LA_ERR_SHAPE
+
+
+@cpu_only
+def test_tile_index_bound_rejected():
+    # 65535 heads x 1 unit x 16384 key blocks x 2 sub-tiles of 64 keys exceeds 32-bit tile indices
+    s = la.make_shape(1, 65535, 128, 16384 * 128, 64, 128)
+    assert la.workspace_bytes(s) == 0
+    # a few heads over 4000 key blocks fit
+    assert la.workspace_bytes(la.make_shape(1, 4, 128, 4000 * 64, 64, 64)) > 0
 
 
 @cpu_only
@@ -100,6 +113,15 @@ def test_bad_arguments_rejected():
     assert att(ctypes.byref(s), p, p, p, p, p, ctypes.c_float(float("inf")), p, None, p, ws, None) == la.LA_ERR_ARG
     assert att(ctypes.byref(s), p, p, p, p, p, ctypes.c_float(0), odd, None, p, ws, None) == la.LA_ERR_ARG
     assert lib.la_mask_to_list(ctypes.byref(s), None, p, p, None) == la.LA_ERR_ARG
+    assert lib.la_sparse_attn_plan(ctypes.byref(s), None, p, p, ws, None) == la.LA_ERR_ARG
+    assert lib.la_sparse_attn_plan(ctypes.byref(s), p, p, None, ws, None) == la.LA_ERR_WORKSPACE
+    assert lib.la_sparse_attn_plan(ctypes.byref(s), p, p, p, 255, None) == la.LA_ERR_WORKSPACE
+    run = lib.la_sparse_attn_run
+    assert run(ctypes.byref(s), p, None, p, ctypes.c_float(0), p, None, p, ws, None) == la.LA_ERR_ARG
+    assert run(ctypes.byref(s), p, p, p, ctypes.c_float(float("nan")), p, None, p, ws, None) == la.LA_ERR_ARG
+    assert run(ctypes.byref(s), p, p, p, ctypes.c_float(0), p, None, p, 16, None) == la.LA_ERR_WORKSPACE
+    assert lib.la_sparse_attn_merge(ctypes.byref(s), None, None, p, ws, None) == la.LA_ERR_ARG
+    assert lib.la_sparse_attn_merge(ctypes.byref(s), odd, None, p, ws, None) == la.LA_ERR_ARG
 
 
 def test_binding_refuses_cpu_tensors():

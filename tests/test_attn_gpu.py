@@ -178,3 +178,33 @@ def test_attn_deterministic_and_split_consistent():
     o2 = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, wl.block)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2)
+
+
+def test_attn_plan_run_merge_equal_fwd():
+    # the three steps give bit-identical o and lse; one plan serves a second run with other q, v
+    B, H, Lq, Lk, d, block = 1, 3, 700, 2100, 128, 64
+    inp = make_clustered(B, H, Lq, Lk, d, block, 12)
+    rng = np.random.default_rng(12)
+    NQ, NK = -(-Lq // block), -(-Lk // block)
+    mask = (rng.uniform(size=(B, H, NQ, NK)) < 0.4).astype(np.uint8)
+    g = to_gpu(inp)
+    counts, idx = la.mask_to_list(torch.from_numpy(mask).cuda(), block, Lq, Lk, d)
+    o1, lse1 = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, block, want_lse=True)
+    shape = la.make_shape(B, H, Lq, Lk, d, block)
+    ws = torch.empty(la.workspace_bytes(shape), dtype=torch.uint8, device="cuda")
+    o2 = torch.empty_like(g["q"])
+    lse2 = torch.empty_like(lse1)
+    plan, run, merge = la.bind_attn_steps(g["q"], g["k"], g["v"], counts, idx, block, o2, ws, lse=lse2)
+    plan()
+    run()
+    merge()
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(lse1, lse2)
+    q2 = (g["q"].float() * 0.5).to(torch.bfloat16)
+    v2 = (g["v"].float() * -2.0).to(torch.bfloat16)
+    o3 = la.sparse_attn_fwd(q2, g["k"], v2, counts, idx, block)
+    run2, merge2 = la.bind_attn_steps(q2, g["k"], v2, counts, idx, block, o2, ws, lse=lse2)[1:]
+    run2()
+    merge2()
+    torch.cuda.synchronize()
+    assert torch.equal(o3, o2)
