@@ -17,20 +17,21 @@
 //
 // The workgroup: 8 waves = two groups of four, one wave of each group per SIMD.  Each wave owns
 // 32 query rows; the two waves of a SIMD own the two halves of the same query block, so both
-// groups own the same tiles.  The groups alternate, offset by one phase and separated by
-// workgroup barriers:
+// groups own the same tiles.  Per tile h the groups run two phases each, offset by one phase and
+// separated by workgroup barriers:
 //
 //   phase    group 0                              group 1
-//   A(h)     M(h): P.V of tile h-1, Q.K^T of h    V(h-1): softmax of tile h-1, loads K(h+2)
-//   B(h)     V(h): softmax of tile h, loads V(h+1) M(h): P.V of tile h-1, Q.K^T of tile h
+//   A(h)     M(h): P.V of tile h-1, Q.K^T of h    V(h-1): softmax of tile h-1, then issues the
+//                                                 loads of K(h+1) and V(h)
+//   B(h)     V(h): softmax of tile h              M(h): P.V of tile h-1, Q.K^T of tile h, then
+//                                                 waits for its loads
 //
 // so on every SIMD one wave feeds the matrix pipeline while the other does the softmax
-// arithmetic, and the asynchronous buffer-to-LDS tile loads are spread among that arithmetic
-// in both phases.  K and V live in three-stage LDS rings: K(h) is read in A(h) and B(h), V(h)
-// in A(h+1) and B(h+1), so K(h+2) and V(h+1) can be written from A(h) on.  A group waits for
-// the loads it issued one V phase earlier at the end of its next V phase (vmcnt: all but the
-// loads just issued).  The loads' buffer descriptors end at Lk, so the ragged last block reads
-// zeros past the end.
+// arithmetic.  K and V have two LDS stages each: K(h) in stage h & 1 is read in A(h) and B(h);
+// V(h) in stage h & 1 is read in A(h+1) and B(h+1); the loads of K(h+1) and V(h), issued in
+// A(h), overwrite the stages last read in B(h-1).  Only group 1 issues tile loads (asynchronous
+// buffer-to-LDS, 16 bytes per lane); their buffer descriptors end at Lk, so the ragged last
+// block reads zeros past the end.
 //
 // Per wave and 64-key tile (d = 128):
 //   S^T (64 keys x 32 queries) = K_tile (64 x d) . Q^T       16 x v_mfma_f32_32x32x16_bf16
