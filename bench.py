@@ -49,10 +49,16 @@ def parse():
 
 
 def src_digest(*names) -> str:
+    """Digest of kernel sources with comments and blank space removed: a change of the code
+    changes it, a change of a comment does not."""
+    import re
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(ROOT, "paper_2605_31158_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2605_31158_amd", "csrc", n)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
