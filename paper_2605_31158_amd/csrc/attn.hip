@@ -56,7 +56,6 @@ constexpr int KT = 64;          // keys per tile
 constexpr int QW = 32;          // query rows per wave
 constexpr int QR = 256;         // query rows per unit (workgroup)
 constexpr int kMaxPersist = 256;        // persistent workgroups: one per CU, at most 256
-constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the running max is raised
 // flags of a tile record (see TileRef)
 constexpr int kFlFrom0 = 1 << 4, kFlToEnd = 1 << 5, kFlFirst = 1 << 6, kFlLast = 1 << 7, kFlValid = 1 << 8;
 
@@ -237,13 +236,10 @@ __device__ __forceinline__ void pv_tile(const unsigned char* __restrict__ vb, co
   __builtin_amdgcn_sched_group_barrier(kSgMfma, AHEAD, 0);
 }
 
-// Masks (ragged tail, frame-causal pairs), running max and the lazy rescale of O for one tile.
-// Lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row (column l%32); the
-// two lanes l and l^32 together hold the row's 64 keys.
-template <int D>
-__device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& m_run, float& l_run, int key0,
-                                             const WaveCtx& w) {
-  constexpr int DT = D / 32;
+// Masks of one tile (ragged tail, frame-causal pairs): invisible keys get -inf.  Lane holds keys
+// key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row (column l%32); the two lanes l and
+// l^32 together hold the row's 64 keys.
+__device__ __forceinline__ void mask_tile(f32x16* sacc, int key0, const WaveCtx& w) {
   if (key0 + KT > w.klimit_wave) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -253,38 +249,12 @@ __device__ __forceinline__ void softmax_prep(f32x16* sacc, f32x16* oacc, float& 
         if (key >= w.klimit) sacc[kt][i] = -INFINITY;
       }
   }
-  float mx = -INFINITY;
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
-  // lanes l and l^32: the swap gives every lane both halves' values
-  const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, mx), __builtin_bit_cast(uint32_t, mx),
-                                                   false, false);
-  mx = fmaxf(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
-  const float mt = mx * w.scale_log2;
-  const bool raise = mt > m_run + kRescaleSlack;
-  if (__any(raise)) {
-    const float m_new = raise ? mt : m_run;
-    const float alpha = raise ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-    m_run = m_new;
-    l_run *= alpha;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
-  }
 }
 
-// P = 2^(S*scale - m) rounded to bf16 into the four B operands of the P.V product; the row
-// sums are taken in fp32 before rounding and added to l_run when `use` (a wave that does not
-// own the tile runs the same straight-line code on stale scores and drops the result).  The NL
-// tile loads of `ld` are spread among the arithmetic.
-template <int NL>
-__device__ __forceinline__ void softmax_p(const f32x16* sacc, bf16x8* pb, float m_run, float& l_run,
-                                          float scale_log2, bool use, const LoadSet<NL>& ld) {
-  constexpr int NV = 112;                // VALU per tile: 32 fma + 32 exp + 32 add + 16 cvt
-  const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+// P = 2^(S*scale - m) rounded to bf16 into the four B operands of the P.V product; returns the
+// lane's sum of its 32 values (fp32, before rounding).
+__device__ __forceinline__ float softmax_exp(const f32x16* sacc, bf16x8* pb, float m, float scale_log2) {
+  const float m_use = (m == -INFINITY) ? 0.f : m;
   float rs0 = 0.f, rs1 = 0.f;
 #pragma unroll
   for (int s4 = 0; s4 < 4; ++s4) {
@@ -299,16 +269,46 @@ __device__ __forceinline__ void softmax_p(const f32x16* sacc, bf16x8* pb, float 
     }
     pb[s4] = __builtin_bit_cast(bf16x8, pw);
   }
+  return rs0 + rs1;
+}
+
+// Softmax of one tile with a lazily raised running max (base 2).  P is first formed against the
+// current max m_run, which is left alone while every lane's sum of its 32 values stays within
+// 2^8 (so no value exceeds 2^8 and the O accumulators keep their range); otherwise, and on the
+// first tile of a piece, the row max of the tile is taken, m_run raised to it, O and l rescaled,
+// and P formed again.  Most tiles thus skip both the row max and the rescale.  A wave that does
+// not own the tile (use false) runs the first pass on stale scores and drops the result.
+template <int D>
+__device__ __forceinline__ void softmax_tile(f32x16* sacc, bf16x8* pb, f32x16* oacc, float& m_run, float& l_run,
+                                             float scale_log2, bool use) {
+  constexpr int DT = D / 32;
+  float rs = softmax_exp(sacc, pb, m_run, scale_log2);
+  const bool redo = use && (m_run == -INFINITY || !(rs <= 256.f));
+  if (__any(redo)) {
+    if (use) {
+      float mx = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < NL; ++j) ld.issue(j);
-  if constexpr (NL > 0) {
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-    for (int j = 0; j < NL; ++j) {
-      __builtin_amdgcn_sched_group_barrier(kSgValu, NV / (NL + 1), 0);
-      __builtin_amdgcn_sched_group_barrier(kSgVmemRead, 1, 0);
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[kt][i]);
+      // lanes l and l^32: the swap gives every lane both halves' values
+      const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, mx),
+                                                       __builtin_bit_cast(uint32_t, mx), false, false);
+      mx = fmaxf(__builtin_bit_cast(float, (uint32_t)sw[0]), __builtin_bit_cast(float, (uint32_t)sw[1]));
+      const float mt = mx * scale_log2;
+      if (mt > m_run) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - mt);   // 0 while m_run is -inf
+        m_run = mt;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+      }
     }
+    rs = softmax_exp(sacc, pb, m_run, scale_log2);
   }
-  l_run += use ? rs0 + rs1 : 0.f;
+  l_run += use ? rs : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -640,13 +640,12 @@ __device__ __forceinline__ void m_phase(WaveState<D>& st, WaveCtx& w, int prev_f
   if (cur.valid() && cur.owned(ka.my_list) && st.rows) qk_tile<D>(kcur, st.qreg, st.sacc, w.kbase);
 }
 
-// V phase of tile `cur`: masks, running max, rescale, P, with the tile loads `ld` spread in.
-template <int D, int NL>
-__device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, const TileRef& cur, const KArgs& ka,
-                                        const LoadSet<NL>& ld) {
+// V phase of tile `cur`: masks, softmax, P.
+template <int D>
+__device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, const TileRef& cur, const KArgs& ka) {
   const bool use = cur.valid() && cur.owned(ka.my_list) && st.rows;
-  if (use) softmax_prep<D>(st.sacc, st.oacc, st.m_run, st.l_run, cur.key0, w);
-  softmax_p<NL>(st.sacc, st.pb, st.m_run, st.l_run, w.scale_log2, use, ld);
+  if (use) mask_tile(st.sacc, cur.key0, w);
+  softmax_tile<D>(st.sacc, st.pb, st.oacc, st.m_run, st.l_run, w.scale_log2, use);
 }
 
 template <int D>
@@ -755,7 +754,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // (scalar load) at the start of each V phase and decoded at its end, so that no scalar load is
   // outstanding during an M phase (it would force the LDS operand reads there to wait for all
   // LDS traffic).  Two iterations per trip, so that every buffer is a compile-time choice.
-  const LoadSet<0> none{TileLoad{}, 0, nullptr};
   auto run = [&](auto G1) {
     constexpr bool IS_G1 = decltype(G1)::value;
     TileRef nx2;
@@ -764,12 +762,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         m_phase<D>(st, w, prev_fl, cur, kc, vp, ka);
         lds_barrier();
         const int4 raw = load_tile(trec, t_begin + hh + 2, t_end);
-        v_phase<D, 0>(st, w, cur, ka, none);
+        v_phase<D>(st, w, cur, ka);
         nx2 = make_tile(raw, t_begin + hh + 2, t_begin, t_end);
         lds_barrier();
       } else {
         const int4 raw = load_tile(trec, t_begin + hh + 2, t_end);
-        v_phase<D, 0>(st, w, TileRef{prev_key0, 0, 0, prev_fl}, ka, none);
+        v_phase<D>(st, w, TileRef{prev_key0, 0, 0, prev_fl}, ka);
         nx2 = make_tile(raw, t_begin + hh + 2, t_begin, t_end);
         issue_loads(kn, nxt, vc, cur);
         barrier_keep_loads();
