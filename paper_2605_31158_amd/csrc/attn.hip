@@ -99,17 +99,18 @@ __device__ __forceinline__ void wait_vmem() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | n);   // vmcnt(n), expcnt and lgkmcnt left at their maximum
 }
 
-// LDS layout: K and V tiles of 64 key rows of D bf16, row-major with padded rows.  K rows are
-// padded to D*2 + 16 bytes: the 32 key rows an MFMA operand read touches (16 per LDS cycle)
-// start in distinct 16-byte bank groups.  V rows are padded to D*2 + 64 bytes: a transpose
-// read touches 4 rows x 64 contiguous bytes per half-wave, which then cover all 64 banks once.
-// Every operand read is then a lane base address plus a compile-time offset.  A tile is
-// written by wave-wide 16-byte-per-lane loads (1 KiB each) of consecutive 16-byte slots;
-// padding slots read as zero.
+// LDS layout: K and V tiles of 64 key rows of D bf16, row-major.  K rows are padded to D*2 + 16
+// bytes: the 32 key rows an MFMA operand read touches (16 per LDS cycle) start in distinct
+// 16-byte bank groups.  V rows are not padded; instead the 64-byte chunks of a row are permuted
+// (chunk c of row r is stored at chunk c ^ vswz(r)): a transpose read touches 4 consecutive rows
+// x 64 contiguous bytes per half-wave, and the permutation spreads those four pieces over all 64
+// banks.  Every K operand read is a lane base plus a compile-time offset, every V read one of
+// D/32 lane bases (base ^ 64 dt) plus a compile-time offset.  A tile is written by wave-wide
+// 16-byte-per-lane loads (1 KiB each) of consecutive 16-byte slots; K padding slots read as zero.
 template <int D>
 struct Tile {
   static constexpr int KSTRIDE = D * 2 + 16;
-  static constexpr int VSTRIDE = D * 2 + 64;
+  static constexpr int VSTRIDE = D * 2;
   static constexpr int KSLOTS = KSTRIDE / 16;          // 16-byte slots per K row
   static constexpr int VSLOTS = VSTRIDE / 16;
   static constexpr int KBYTES = KT * KSTRIDE;
@@ -119,6 +120,9 @@ struct Tile {
   static constexpr int KPER = KINST / 4;               // per loading wave (wave 0 loads one more)
   static constexpr int VPER = VINST / 4;
   static_assert(KINST % 4 == 1 && VINST % 4 == 0, "load split");
+  // chunk permutation of V row r: rows 4i..4i+3 get four distinct chunks (D = 128: 4 chunks per
+  // row) or, with 128-byte rows (D = 64), rows 4i, 4i+2 and 4i+1, 4i+3 get opposite chunks
+  __device__ static constexpr int vswz(int r) { return D == 128 ? (r & 3) : ((r >> 1) & 1); }
 };
 
 // Global byte offset (inside a tile of 64 rows) that lane `lane` of load `n` fetches so that it
@@ -129,6 +133,17 @@ __device__ inline uint32_t slot_offset(int n, int lane, int slots) {
   const int slot = 64 * n + lane;
   const int row = slot / slots, chunk = slot % slots;
   return chunk < D / 8 ? (uint32_t)(row * D * 2 + chunk * 16) : 0x7fffffffu;
+}
+
+// The same for the V layout: LDS slot 64 n + lane holds part w (16 bytes) of stored chunk pc of
+// row r, i.e. logical chunk pc ^ vswz(r).
+template <int D>
+__device__ inline uint32_t vslot_offset(int n, int lane) {
+  constexpr int SL = D / 8;
+  const int slot = 64 * n + lane;
+  const int row = slot / SL, sp = slot % SL;
+  const int chunk = (sp >> 2) ^ Tile<D>::vswz(row);
+  return (uint32_t)(row * D * 2 + chunk * 64 + (sp & 3) * 16);
 }
 
 // Loads of one tile of one matrix by one loading wave: a buffer descriptor that starts at the
@@ -207,7 +222,8 @@ __device__ __forceinline__ void qk_tile(const unsigned char* __restrict__ kb, co
 }
 
 // O^T += V^T P^T for one 64-key tile (P in four bf16 B operands of 16 keys each).  The two
-// transpose reads of each V^T operand run two MFMAs ahead of their use.
+// transpose reads of each V^T operand run two MFMAs ahead of their use.  Column block dt of the
+// lane's rows sits at vbase ^ (64 dt) (see Tile).
 template <int D>
 __device__ __forceinline__ void pv_tile(const unsigned char* __restrict__ vb, const bf16x8* pb, f32x16* oacc,
                                         int vbase) {
@@ -219,7 +235,7 @@ __device__ __forceinline__ void pv_tile(const unsigned char* __restrict__ vb, co
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     const int s4 = i / DT, dt = i % DT;
-    const unsigned char* vp = vb + vbase + (16 * s4) * T::VSTRIDE + 64 * dt;
+    const unsigned char* vp = vb + (vbase ^ (64 * dt)) + (16 * s4) * T::VSTRIDE;
     const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(vp));
     const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(vp + 8 * T::VSTRIDE));
     const v8i16 a8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -705,11 +721,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
   for (int j = 0; j <= T::KPER; ++j) koff[j] = slot_offset<D>(j < T::KPER ? lw + 4 * j : 4 * T::KPER, lane, T::KSLOTS);
 #pragma unroll
-  for (int j = 0; j < T::VPER; ++j) voff[j] = slot_offset<D>(lw + 4 * j, lane, T::VSLOTS);
+  for (int j = 0; j < T::VPER; ++j) voff[j] = vslot_offset<D>(lw + 4 * j, lane);
   WaveCtx w;
   w.key_lk = gm.Lk;
   w.kbase = c32 * T::KSTRIDE + 16 * h;
-  w.vbase = (4 * h + ((lane & 15) >> 2)) * T::VSTRIDE + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
+  {
+    const int vrow = 4 * h + ((lane & 15) >> 2);   // + multiples of 8 rows in the immediates
+    w.vbase = vrow * T::VSTRIDE + 64 * T::vswz(vrow) + 32 * ((lane >> 4) & 1) + 8 * (lane & 3);
+  }
   w.h = h;
   w.scale_log2 = scale_log2;
   w.klimit = gm.Lk;
