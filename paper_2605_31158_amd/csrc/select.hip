@@ -13,7 +13,7 @@
 //                 M scores, then a radix select over the 32-bit order keys of the scores (4
 //                 passes of 8 bits, per-wave LDS histogram) that finds the score at which the
 //                 mass, accumulated from the highest score down, first reaches tau (or the
-//                 count reaches the top-k size).  Masses are 2^-32 fixed-point integers, so the
+//                 count reaches the top-k size).  Masses are 2^-31 fixed-point integers, so the
 //                 sums are exact and independent of summation order.  Equal scores at the
 //                 cutoff are taken in ascending block order.  The kept set is merged with the
 //                 forced blocks and emitted, ascending, with lane ballots: mask row, count, list.
@@ -162,18 +162,6 @@ __global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const uint1
   }
 }
 
-// ---------------------------------------------------------------------------
-// 64-bit lane shuffles
-
-__device__ inline uint64_t shfl_xor_u64(uint64_t x, int off) {
-  const uint32_t lo = __shfl_xor((uint32_t)x, off), hi = __shfl_xor((uint32_t)(x >> 32), off);
-  return ((uint64_t)hi << 32) | lo;
-}
-__device__ inline uint64_t shfl_up_u64(uint64_t x, int off) {
-  const uint32_t lo = __shfl_up((uint32_t)x, off), hi = __shfl_up((uint32_t)(x >> 32), off);
-  return ((uint64_t)hi << 32) | lo;
-}
-
 // Order key: ascending key = score descending.  -0 and +0 map to the same key.
 __device__ inline uint32_t order_key(float s) {
   if (s == 0.0f) s = 0.0f;
@@ -195,20 +183,6 @@ __device__ inline float wave_sum(float x) {
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
   return x;
 }
-__device__ inline uint64_t wave_sum_u64(uint64_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += shfl_xor_u64(x, off);
-  return x;
-}
-__device__ inline uint64_t wave_incl_scan_u64(uint64_t x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint64_t y = shfl_up_u64(x, off);
-    if (lane >= off) x += y;
-  }
-  return x;
-}
 __device__ inline uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
 // All LDS operations this wave issued have completed before the next one starts.
@@ -226,75 +200,108 @@ __device__ inline void emit_range(int lo, int hi, int pos, uint8_t* mask_row, in
   }
 }
 
-constexpr double kFix = 4294967296.0;   // 2^32 fixed-point scale of the mass
+constexpr float kFix = 2147483648.0f;   // 2^31 fixed-point scale of the mass (sums fit 32 bits)
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ inline uint32_t wave_sum_u32(uint32_t x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+__device__ inline uint32_t wave_min_u32(uint32_t x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = min(x, (uint32_t)__shfl_xor(x, off));
+  return x;
+}
+__device__ inline uint32_t wave_max_u32(uint32_t x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = max(x, (uint32_t)__shfl_xor(x, off));
+  return x;
+}
+__device__ inline uint32_t wave_incl_scan_u32(uint32_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
 
 // One wave per (head, query block).  Lane l holds candidates m = l + 64 j, j < NPER.
+// Masses are floor(p * 2^31) (tau rule) or 1 per candidate (top-k rule); their sum over a row
+// stays below 2^32.
 template <int NPER>
 __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __restrict__ scores, int NQ,
                                                                int NK, int M, int h0, int h1, float tau,
                                                                int keep_fixed, uint8_t* __restrict__ mask,
                                                                int32_t* __restrict__ counts,
                                                                int32_t* __restrict__ idx) {
-  __shared__ uint64_t hist_all[kThreads / 64][256];
+  __shared__ uint32_t hist_all[kThreads / 64][256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x * (kThreads / 64) + wave;
   const int bh = blockIdx.y;
   if (i >= NQ) return;
-  uint64_t* hist = hist_all[wave];
+  uint32_t* hist = hist_all[wave];
   const size_t row = (size_t)bh * NQ + i;
   const float* s = scores + row * (size_t)M;
   uint8_t* mask_row = mask ? mask + row * (size_t)NK : nullptr;
   int32_t* idx_row = idx + row * (size_t)NK;
 
-  float sv[NPER];
-  uint32_t w[NPER];
-#pragma unroll
-  for (int j = 0; j < NPER; ++j) {
-    const int m = lane + 64 * j;
-    sv[j] = m < M ? s[m] : -FLT_MAX;
-  }
-  // mode: keep all / keep none / select
+  uint32_t uk[NPER];    // order keys
+  uint32_t w[NPER];     // masses
   bool keep_all = keep_fixed < 0 ? tau >= 1.0f : keep_fixed >= M;
-  uint64_t target = 0;
-  if (!keep_all) {
-    if (keep_fixed >= 0) {
+  uint32_t target = 0;
+  {
+    float sv[NPER];
 #pragma unroll
-      for (int j = 0; j < NPER; ++j) w[j] = (lane + 64 * j < M) ? 1u : 0u;
-      target = (uint64_t)keep_fixed;
-    } else {
-      float mx = -FLT_MAX;
-#pragma unroll
-      for (int j = 0; j < NPER; ++j) mx = fmaxf(mx, sv[j]);
-      mx = wave_max(mx);
-      float e[NPER];
-      float sum = 0.f;
-#pragma unroll
-      for (int j = 0; j < NPER; ++j) {
-        e[j] = (lane + 64 * j < M) ? expf(sv[j] - mx) : 0.f;
-        sum += e[j];
-      }
-      sum = wave_sum(sum);
-#pragma unroll
-      for (int j = 0; j < NPER; ++j) {
-        const double f = (double)(e[j] / sum) * kFix;
-        w[j] = f >= 4294967295.0 ? 0xffffffffu : (uint32_t)f;
-      }
-      target = (uint64_t)((double)tau * kFix);
-      if (target == 0) target = 1;     // any tau > 0 keeps at least the top candidate
+    for (int j = 0; j < NPER; ++j) {
+      const int m = lane + 64 * j;
+      sv[j] = m < M ? s[m] : -FLT_MAX;
     }
-    uint64_t wl = 0;
+    if (!keep_all) {
+      if (keep_fixed >= 0) {
 #pragma unroll
-    for (int j = 0; j < NPER; ++j) wl += w[j];
-    if (wave_sum_u64(wl) < target) keep_all = true;   // the mass / count never reaches the target
+        for (int j = 0; j < NPER; ++j) w[j] = (lane + 64 * j < M) ? 1u : 0u;
+        target = (uint32_t)keep_fixed;
+      } else {
+        // softmax over the M candidates: exp(s - max) = 2^((s - max) log2 e); every term <= 1
+        // and the sum >= 1, so floor(e * 2^31 / sum) <= 2^31
+        float mx = -FLT_MAX;
+#pragma unroll
+        for (int j = 0; j < NPER; ++j) mx = fmaxf(mx, sv[j]);
+        mx = wave_max(mx);
+        float e[NPER];
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < NPER; ++j) {
+          e[j] = (lane + 64 * j < M) ? __builtin_amdgcn_exp2f((sv[j] - mx) * kLog2e) : 0.f;
+          sum += e[j];
+        }
+        sum = wave_sum(sum);
+        const float sc = kFix / sum;
+#pragma unroll
+        for (int j = 0; j < NPER; ++j) w[j] = (uint32_t)(e[j] * sc);
+        target = (uint32_t)(tau * kFix);
+        if (target == 0) target = 1;     // any tau > 0 keeps at least the top candidate
+      }
+      uint32_t wl = 0;
+#pragma unroll
+      for (int j = 0; j < NPER; ++j) wl += w[j];
+      if (wave_sum_u32(wl) < target) keep_all = true;   // the mass / count never reaches the target
+    }
+#pragma unroll
+    for (int j = 0; j < NPER; ++j) uk[j] = order_key(sv[j]);
   }
   // cutoff: smallest order key u* whose inclusive weight reaches the target (radix select,
-  // 4 passes of 8 bits over a per-wave 256-bin histogram), then equal keys by block index
+  // passes of 8 bits over a per-wave 256-bin histogram; after the second pass, a crossing bin
+  // whose candidates all share one key ends the search), then equal keys by block index
   uint32_t ustar = 0xffffffffu;
   int mstar = 0x7fffffff;
   const bool none = !keep_all && target == 0;
   if (!keep_all && !none) {
-    uint32_t prefix = 0;
-    uint64_t before = 0;
+    uint32_t prefix = 0, before = 0;
+    bool found = false;
     for (int pass = 0; pass < 4; ++pass) {
       const int shift = 24 - 8 * pass;
 #pragma unroll
@@ -302,49 +309,63 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
       wave_lds_sync();
 #pragma unroll
       for (int j = 0; j < NPER; ++j) {
-        const uint32_t uk = order_key(sv[j]);
-        const bool in = w[j] != 0 && (pass == 0 || (uk >> (shift + 8)) == prefix);
-        if (in) atomicAdd((unsigned long long*)&hist[(uk >> shift) & 255u], (unsigned long long)w[j]);
+        const bool in = w[j] != 0 && (pass == 0 || (uk[j] >> (shift + 8)) == prefix);
+        if (in) atomicAdd(&hist[(uk[j] >> shift) & 255u], w[j]);
       }
       wave_lds_sync();
-      uint64_t b4[4];
-      uint64_t loc = 0;
+      uint32_t b4[4];
+      uint32_t loc = 0;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         loc += hist[4 * lane + t];
         b4[t] = loc;
       }
-      const uint64_t excl = wave_incl_scan_u64(loc) - loc;
+      const uint32_t excl = wave_incl_scan_u32(loc) - loc;
       int hit = -1;
 #pragma unroll
       for (int t = 3; t >= 0; --t)
         if (before + excl + b4[t] >= target) hit = t;
       const unsigned long long bal = __ballot(hit >= 0);
       const int first = __ffsll(bal) - 1;              // lane holding the crossing bin
-      const uint64_t below = before + excl + (hit > 0 ? b4[hit > 0 ? hit - 1 : 0] : 0);
+      const uint32_t below = before + excl + (hit > 0 ? b4[hit > 0 ? hit - 1 : 0] : 0);
       const int bin = 4 * lane + hit;
       prefix = (prefix << 8) | (uint32_t)__shfl(bin, first);
-      before = ((uint64_t)(uint32_t)__shfl((uint32_t)(below >> 32), first) << 32) |
-               (uint32_t)__shfl((uint32_t)below, first);
+      before = (uint32_t)__shfl(below, first);
+      if (pass == 1) {
+        uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+        for (int j = 0; j < NPER; ++j) {
+          if (w[j] != 0 && (uk[j] >> shift) == prefix) {
+            kmin = min(kmin, uk[j]);
+            kmax = max(kmax, uk[j]);
+          }
+        }
+        kmin = wave_min_u32(kmin);
+        if (kmin == wave_max_u32(kmax)) {
+          ustar = kmin;
+          found = true;
+          break;
+        }
+      }
     }
-    ustar = prefix;
+    if (!found) ustar = prefix;
     int ntie = 0;
 #pragma unroll
-    for (int j = 0; j < NPER; ++j) ntie += (w[j] != 0 && order_key(sv[j]) == ustar) ? 1 : 0;
-    if ((int)wave_sum((float)ntie) > 1) {
+    for (int j = 0; j < NPER; ++j) ntie += (w[j] != 0 && uk[j] == ustar) ? 1 : 0;
+    if (wave_sum_u32((uint32_t)ntie) > 1) {
       // equal scores at the cutoff: take them in ascending block order until the target
-      uint64_t base = before;
+      uint32_t base = before;
 #pragma unroll
       for (int j = 0; j < NPER; ++j) {
-        const uint64_t wt = (w[j] != 0 && order_key(sv[j]) == ustar) ? w[j] : 0;
-        const uint64_t incl = wave_incl_scan_u64(wt);
+        const uint32_t wt = (w[j] != 0 && uk[j] == ustar) ? w[j] : 0;
+        const uint32_t incl = wave_incl_scan_u32(wt);
         const bool cross = wt != 0 && base + incl >= target && base + incl - wt < target;
         const unsigned long long bal = __ballot(cross);
         if (bal) {
           mstar = 64 * j + __ffsll(bal) - 1;
           break;
         }
-        base += (uint64_t)__shfl((uint32_t)incl, 63) | ((uint64_t)(uint32_t)__shfl((uint32_t)(incl >> 32), 63) << 32);
+        base += (uint32_t)__shfl(incl, 63);
       }
     }
   }
@@ -357,10 +378,7 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
     bool kept = false;
     if (m < M) {
       if (keep_all) kept = true;
-      else if (!none) {
-        const uint32_t uk = order_key(sv[j]);
-        kept = w[j] != 0 && (uk < ustar || (uk == ustar && m <= mstar));
-      }
+      else if (!none) kept = w[j] != 0 && (uk[j] < ustar || (uk[j] == ustar && m <= mstar));
       if (mask_row) mask_row[h0 + m] = kept ? 1 : 0;
     }
     const unsigned long long bal = __ballot(kept);
