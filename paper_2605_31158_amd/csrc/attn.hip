@@ -853,7 +853,6 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
     const int64_t lam = ((int64_t)(t + 1) * P + Ttot - 1) / Ttot - 1;
     return (int)(lam < P - 1 ? lam : P - 1);
   };
-  const int la1 = owner(te - 1);
   const int bh = u / row_tiles;
   const int cg = threadIdx.x % CG, r0 = blockIdx.y * kCombRows + threadIdx.x / CG;
   float m[NI], l[NI];
@@ -864,23 +863,29 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
     l[i] = 0.f;
     acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // streams with an empty range (fewer tiles than streams) wrote no slot
-  for (int lam = lam0; lam <= la1; ++lam) {
-    if (range_begin(Ttot, lam, P) == range_begin(Ttot, lam + 1, P)) continue;
-    const int slot = lam == lam0 ? 2 * lam + 1 : 2 * lam;
+  // The pieces of the unit, in stream order: the last piece of this range (slot 2 lam0 + 1),
+  // then one piece in each later non-empty range up to the one holding tile te - 1 (slot 2 lam:
+  // the first piece of that range).  Streams are visited through the tiles they hold, so empty
+  // ranges (fewer tiles than streams) cost nothing.
+  for (int pass = 0; pass < 2; ++pass) {
+    int lam = lam0, next = e;
+    while (true) {
+      const int slot = lam == lam0 ? 2 * lam + 1 : 2 * lam;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) m[i] = fmaxf(m[i], part_m[(size_t)slot * QR + r0 + RSTEP * i]);
-  }
-  for (int lam = lam0; lam <= la1; ++lam) {
-    if (range_begin(Ttot, lam, P) == range_begin(Ttot, lam + 1, P)) continue;
-    const int slot = lam == lam0 ? 2 * lam + 1 : 2 * lam;
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const size_t pr = (size_t)slot * QR + r0 + RSTEP * i;
-      const float wgt = exp2f(part_m[pr] - (m[i] == -INFINITY ? 0.f : m[i]));
-      l[i] += wgt * part_l[pr];
-      const f32x4 po = *(const f32x4*)(part_o + pr * D + 4 * cg);
-      acc[i] += wgt * po;
+      for (int i = 0; i < NI; ++i) {
+        const size_t pr = (size_t)slot * QR + r0 + RSTEP * i;
+        if (pass == 0) {
+          m[i] = fmaxf(m[i], part_m[pr]);
+        } else {
+          const float wgt = exp2f(part_m[pr] - (m[i] == -INFINITY ? 0.f : m[i]));
+          l[i] += wgt * part_l[pr];
+          const f32x4 po = *(const f32x4*)(part_o + pr * D + 4 * cg);
+          acc[i] += wgt * po;
+        }
+      }
+      if (next >= te) break;
+      lam = owner(next);
+      next = range_begin(Ttot, lam + 1, P);
     }
   }
 #pragma unroll
