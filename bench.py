@@ -48,18 +48,22 @@ def parse():
     return ap.parse_args()
 
 
-def src_digest(*names) -> str:
-    """Digest of kernel sources with comments and blank space removed: a change of the code
+def code_digest(text: str) -> str:
+    """Digest of C/C++ source text with comments and blank space removed: a change of the code
     changes it, a change of a comment does not."""
     import re
-    h = hashlib.sha256()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()[:16]
+
+
+def src_digest(*names) -> str:
+    """code_digest of the named kernel sources (paper_2605_31158_amd/csrc), concatenated."""
+    text = ""
     for n in names:
         with open(os.path.join(ROOT, "paper_2605_31158_amd", "csrc", n)) as f:
-            text = f.read()
-        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-        text = re.sub(r"//[^\n]*", "", text)
-        h.update(" ".join(text.split()).encode())
-    return h.hexdigest()[:16]
+            text += f.read() + "\n"
+    return code_digest(text)
 
 
 def traffic_from_profile(kernel_tag: str, workload: str, digest: str, launches_bytes: float):
@@ -72,6 +76,16 @@ def traffic_from_profile(kernel_tag: str, workload: str, digest: str, launches_b
     if rec.get("src_digest") != digest:
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def kept_flop_count(mask_np, Lq: int, Lk: int, block: int, d: int) -> int:
+    """4 d x (valid query rows x valid keys) summed over the kept (query block, key block) pairs:
+    the two matrix products over kept blocks."""
+    NQ, NK = mask_np.shape[-2], mask_np.shape[-1]
+    rows = np.minimum(np.arange(1, NQ + 1) * block, Lq) - np.arange(NQ) * block
+    keys = np.minimum(np.arange(1, NK + 1) * block, Lk) - np.arange(NK) * block
+    kept = mask_np.reshape(-1, NQ, NK).astype(np.int64)
+    return int(4 * d * (kept * rows[:, None] * keys[None, :]).sum())
 
 
 def cpu_baseline(wl, inp, mask_np, target_s: float):
@@ -183,10 +197,7 @@ def main():
     t_att = t_plan + t_run + t_merge
 
     mask_np = mask.cpu().numpy()
-    nq_valid = np.array([min((i + 1) * wl.block, Lq) - i * wl.block for i in range(NQ)], np.int64)
-    nk_valid = np.array([min((m + 1) * wl.block, wl.Lk) - m * wl.block for m in range(NK)], np.int64)
-    kept_flops = float(4 * d * np.einsum("xij,i,j->", mask_np.reshape(-1, NQ, NK).astype(np.int64),
-                                         nq_valid, nk_valid))
+    kept_flops = float(kept_flop_count(mask_np, Lq, wl.Lk, wl.block, d))
     dense_flops = 4.0 * B * H * Lq * wl.Lk * d
     rho = kept_flops / dense_flops
 
