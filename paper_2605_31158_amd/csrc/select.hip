@@ -173,15 +173,28 @@ __device__ inline uint32_t order_key(float s) {
 // ---------------------------------------------------------------------------
 // wave-level helpers (one wave per query-block row: no workgroup barriers)
 
+// Wave-wide reductions (every lane gets the result) and the inclusive scan, with DPP row
+// operations and the row-pair / half-wave swaps: no LDS round trip.
+template <typename Op>
+__device__ inline uint32_t wave_allreduce(uint32_t x, Op op) {
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xb1, 0xf, 0xf, false));    // quad_perm 1,0,3,2
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4e, 0xf, 0xf, false));    // quad_perm 2,3,0,1
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x124, 0xf, 0xf, false));   // row_ror:4
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x128, 0xf, 0xf, false));   // row_ror:8
+  const auto r16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);                 // rows 0<->1, 2<->3
+  x = op((uint32_t)r16[0], (uint32_t)r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);                 // halves
+  return op((uint32_t)r32[0], (uint32_t)r32[1]);
+}
 __device__ inline float wave_max(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
-  return x;
+  return __builtin_bit_cast(float, wave_allreduce(__builtin_bit_cast(uint32_t, x), [](uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
+  }));
 }
 __device__ inline float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-  return x;
+  return __builtin_bit_cast(float, wave_allreduce(__builtin_bit_cast(uint32_t, x), [](uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
+  }));
 }
 __device__ inline uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
@@ -204,27 +217,23 @@ constexpr float kFix = 2147483648.0f;   // 2^31 fixed-point scale of the mass (s
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ inline uint32_t wave_sum_u32(uint32_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-  return x;
+  return wave_allreduce(x, [](uint32_t a, uint32_t b) { return a + b; });
 }
 __device__ inline uint32_t wave_min_u32(uint32_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x = min(x, (uint32_t)__shfl_xor(x, off));
-  return x;
+  return wave_allreduce(x, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
 }
 __device__ inline uint32_t wave_max_u32(uint32_t x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x = max(x, (uint32_t)__shfl_xor(x, off));
-  return x;
+  return wave_allreduce(x, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
 }
+// inclusive prefix sum over the lanes: shifts 1, 2, 4, 8 inside each row of 16 lanes, then the
+// last lane of row 0 (2) added to row 1 (3), and the last lane of row 1 to rows 2 and 3
 __device__ inline uint32_t wave_incl_scan_u32(uint32_t x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
   return x;
 }
 
@@ -329,8 +338,8 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
       const int first = __ffsll(bal) - 1;              // lane holding the crossing bin
       const uint32_t below = before + excl + (hit > 0 ? b4[hit > 0 ? hit - 1 : 0] : 0);
       const int bin = 4 * lane + hit;
-      prefix = (prefix << 8) | (uint32_t)__shfl(bin, first);
-      before = (uint32_t)__shfl(below, first);
+      prefix = (prefix << 8) | (uint32_t)__builtin_amdgcn_readlane(bin, first);
+      before = (uint32_t)__builtin_amdgcn_readlane((int)below, first);
       if (pass == 1) {
         uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
@@ -365,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
           mstar = 64 * j + __ffsll(bal) - 1;
           break;
         }
-        base += (uint32_t)__shfl(incl, 63);
+        base += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
       }
     }
   }
