@@ -1,0 +1,82 @@
+"""Parity report over the named workloads (run on a GPU machine; not collected by pytest):
+
+    python tests/parity_report.py [workload ...] > report.md
+
+For every workload: the GPU block mask against the fp64 oracle's (entries that differ, and
+entries that differ outside the ambiguity band), then the GPU attention output on the GPU's
+own mask against the oracle on sampled query blocks (every block for the tiny workload):
+max-abs and mean-abs error of o and max-abs error of lse.  The same checks, with the same
+bars, are asserted by the GPU tests; this script prints the numbers."""
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+from oracle import la_oracle as O  # noqa: E402
+from paper_2605_31158_amd.workloads import WORKLOADS, make_inputs  # noqa: E402
+
+DEFAULT = ["tiny", "480p_window", "480p_memory", "720p", "720p_causal", "480p_long", "480p_long_dense"]
+
+
+def report(name, samples=24):
+    import torch
+    from paper_2605_31158_amd import la
+    wl = WORKLOADS[name]
+    F = wl.frame_tokens if wl.causal_frames else 0
+    inp = make_inputs(wl)
+    g = {x: la.bf16_from_bits(inp[x]) for x in "qkv"}
+    mask, counts, idx = la.select_blocks(g["q"], g["k"], wl.block, wl.tau, n_text=wl.n_text)
+    o, lse = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, wl.block, n_text=wl.n_text,
+                                frame_tokens=F, want_lse=True)
+    torch.cuda.synchronize()
+    mask_np = mask.cpu().numpy()
+    o_np = o.float().cpu().numpy().astype(np.float64)
+    lse_np = lse.cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    sel = O.select_blocks(inp["q"], inp["k"], wl.block, tau=wl.tau, n_text=wl.n_text)
+    t_sel = time.perf_counter() - t0
+    diff = mask_np != sel["mask"]
+    outside = diff & ~O.ambiguous_blocks(sel, 1e-4)
+    B, H, NQ = wl.B, wl.H, wl.nq
+    if NQ * B * H <= 64:
+        rows = [(b, h, i) for b in range(B) for h in range(H) for i in range(NQ)]
+    else:
+        rng = np.random.default_rng(2024)
+        heavy = np.argsort(-mask_np.sum(-1).ravel(), kind="stable")[:4]
+        flat = list(heavy) + list(rng.integers(0, B * H * NQ, size=samples - 6)) + [NQ - 1, B * H * NQ - 1]
+        rows = sorted({(int(f) // (H * NQ), (int(f) // NQ) % H, int(f) % NQ) for f in flat})
+    t0 = time.perf_counter()
+    ref = O.attention_rows(inp["q"], inp["k"], inp["v"], mask_np, wl.block, rows, frame_tokens=F)
+    t_att = time.perf_counter() - t0
+    mx = mean_sum = lse_mx = 0.0
+    n = 0
+    for (b, h, i), (ob, lb) in ref.items():
+        lo = i * wl.block
+        d = np.abs(o_np[b, h, lo:lo + ob.shape[0]] - ob)
+        mx = max(mx, float(d.max()))
+        mean_sum += float(d.sum())
+        n += d.size
+        fin = np.isfinite(lb)
+        if fin.any():
+            lse_mx = max(lse_mx, float(np.abs(lse_np[b, h, lo:lo + ob.shape[0]][fin] - lb[fin]).max()))
+    rho = O.kept_flops(mask_np, wl.Lq, wl.Lk, wl.block, wl.d) / (4.0 * B * H * wl.Lq * wl.Lk * wl.d)
+    print(f"| {name} | {rho:.4f} | {int(diff.sum())} of {diff.size} | {int(outside.sum())} | {len(rows)} | "
+          f"{mx:.2e} | {mean_sum / max(n, 1):.2e} | {lse_mx:.2e} | {t_sel:.1f} / {t_att:.1f} |", flush=True)
+    return int(outside.sum()) == 0 and mx <= 2e-2 and mean_sum / max(n, 1) <= 2e-3
+
+
+def main():
+    names = sys.argv[1:] or DEFAULT
+    print("| workload | kept ratio | mask entries differing | outside the 1e-4 band | query blocks compared | "
+          "o max-abs | o mean-abs | lse max-abs | oracle s (select / attention rows) |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    ok = all([report(n) for n in names])
+    sys.exit(0 if ok else 1)
+
+
+if __name__ == "__main__":
+    main()
