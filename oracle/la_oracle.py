@@ -352,3 +352,114 @@ def kept_flops(mask: np.ndarray, Lq: int, Lk: int, block: int, d: int) -> int:
     nk_valid = np.array([min((m + 1) * block, Lk) - m * block for m in range(NK)], dtype=np.int64)
     m = mask.reshape(-1, NQ, NK).astype(np.int64)
     return int(4 * d * np.einsum("xij,i,j->", m, nq_valid, nk_valid))
+
+
+# ---------------------------------------------------------------------------
+# 3-D blocks (Sec. 3.3: historical visual tokens partitioned into non-overlapping
+# (B_t, B_h, B_w) blocks; text and current-chunk tokens always kept; the appendix's block
+# sizes are (4, 8, 4) and (4, 4, 8), 128 tokens each)
+
+def blocks_3d(T: int, Hs: int, Ws: int, bt: int, bh: int, bw: int, offset: int = 0) -> List[np.ndarray]:
+    """Token positions of the 3-D blocks of a run of T frames of Hs x Ws visual tokens.
+
+    Token (t, y, x) sits at offset + (t * Hs + y) * Ws + x (frames one after another, each in
+    raster order).  Blocks come in raster order of their (t, y, x) block coordinates; a block
+    at a grid edge holds the tokens that exist there.  Inside a block, tokens are listed in
+    raster order.
+    """
+    out = []
+    for t0 in range(0, T, bt):
+        for y0 in range(0, Hs, bh):
+            for x0 in range(0, Ws, bw):
+                idx = [offset + (t * Hs + y) * Ws + x
+                       for t in range(t0, min(t0 + bt, T))
+                       for y in range(y0, min(y0 + bh, Hs))
+                       for x in range(x0, min(x0 + bw, Ws))]
+                out.append(np.array(idx, dtype=np.int64))
+    return out
+
+
+def layout_3d(n_text: int, T_ctx: int, T_q: int, Hs: int, Ws: int, bt: int, bh: int, bw: int,
+              text_block: int) -> Dict[str, object]:
+    """Blocks of one AR chunk with 3-D visual blocks.
+
+    Keys, in linear order: n_text text tokens, T_ctx context frames, T_q chunk frames.  Key
+    blocks: the text in 1-D blocks of text_block tokens, then the 3-D blocks of the context
+    frames, then those of the chunk frames.  Text and chunk blocks are forced; the context
+    blocks are the historical candidates.  Query blocks: the 3-D blocks of the chunk frames,
+    as positions inside the chunk.
+    """
+    F = Hs * Ws
+    ktext = [np.arange(s, min(s + text_block, n_text), dtype=np.int64) for s in range(0, n_text, text_block)]
+    kctx = blocks_3d(T_ctx, Hs, Ws, bt, bh, bw, offset=n_text)
+    kchunk = blocks_3d(T_q, Hs, Ws, bt, bh, bw, offset=n_text + T_ctx * F)
+    ksets = ktext + kctx + kchunk
+    forced = np.array([True] * len(ktext) + [False] * len(kctx) + [True] * len(kchunk), dtype=bool)
+    qsets = blocks_3d(T_q, Hs, Ws, bt, bh, bw, offset=0)
+    return {"qsets": qsets, "ksets": ksets, "forced": forced, "Lq": T_q * F,
+            "Lk": n_text + (T_ctx + T_q) * F}
+
+
+def pool_sets(x: np.ndarray, sets: Sequence[np.ndarray]) -> np.ndarray:
+    """Pooled proxy of every block given by its token positions: the mean over them
+    (Sec. 3.3, pooling equation).  x: [..., L, d] -> [..., len(sets), d]."""
+    x = _as_f64(x)
+    out = np.empty(x.shape[:-2] + (len(sets), x.shape[-1]), dtype=np.float64)
+    for i, idx in enumerate(sets):
+        total = np.zeros(x.shape[:-2] + (x.shape[-1],), dtype=np.float64)
+        for t in idx:
+            total = total + x[..., int(t), :]
+        out[..., i, :] = total / len(idx)
+    return out
+
+
+def select_blocks_sets(q, k, qsets, ksets, forced, tau: Optional[float] = None,
+                       topk_r: Optional[float] = None) -> Dict[str, object]:
+    """Block selection with blocks given as token sets (the 3-D layout); same rules as
+    select_blocks.  Returns the mask [B, H, NQ, NK] and the intermediate values, with a
+    "part" entry shaped like partition()'s."""
+    if (tau is None) == (topk_r is None):
+        raise ValueError("give exactly one of tau and topk_r")
+    q = _as_f64(q)
+    k = _as_f64(k)
+    B, H, _, d = q.shape
+    NQ, NK = len(qsets), len(ksets)
+    forced = np.asarray(forced, dtype=bool)
+    hist = np.nonzero(~forced)[0].astype(np.int64)
+    qbar = pool_sets(q, qsets)
+    kbar = pool_sets(k, [ksets[int(m)] for m in hist])
+    s = block_scores(qbar, kbar, d)
+    mask = np.zeros((B, H, NQ, NK), dtype=np.uint8)
+    rows = {}
+    for b in range(B):
+        for h in range(H):
+            for i in range(NQ):
+                sel = select_tau_row(s[b, h, i], tau) if tau is not None else select_topk_row(s[b, h, i], topk_r)
+                rows[(b, h, i)] = sel
+                mask[b, h, i, forced] = 1
+                mask[b, h, i, hist[sel["selected"]]] = 1
+    part = {"NQ": NQ, "NK": NK, "forced": forced, "hist": hist, "M": int(hist.size)}
+    return {"mask": mask, "scores": s, "qbar": qbar, "kbar": kbar, "rows": rows, "part": part,
+            "tau": tau, "topk_r": topk_r}
+
+
+def attention_sets_rows(q, k, v, qsets, ksets, mask, rows: Iterable[Tuple[int, int, int]],
+                        scale: Optional[float] = None):
+    """Attention of the query tokens of block i over the tokens of its kept key blocks, for
+    selected (b, h, i); every kept key is visible.  Returns {(b, h, i): (o [|Q_i|, d] in the
+    order of qsets[i], lse [|Q_i|])}."""
+    d = q.shape[-1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    out = {}
+    cache = {}
+    for (b, h, i) in rows:
+        if (b, h) not in cache:
+            cache = {(b, h): (_as_f64(q[b, h]), _as_f64(k[b, h]), _as_f64(v[b, h]))}
+        qh, kh, vh = cache[(b, h)]
+        kept = np.nonzero(mask[b, h, i])[0]
+        cand = np.sort(np.concatenate([ksets[int(m)] for m in kept])) if kept.size else np.zeros(0, np.int64)
+        qi = qsets[i]
+        ok = np.ones((qi.size, cand.size), dtype=bool)
+        out[(b, h, i)] = attention_block(qh[qi], kh[cand], vh[cand], ok, scale)
+    return out
