@@ -150,6 +150,99 @@ la_status la_sparse_attn_merge(const la_shape* shape, void* o, float* lse, void*
 la_status la_mask_to_list(const la_shape* shape, const uint8_t* mask, int32_t* counts,
                           int32_t* idx, void* stream);
 
+/* ------------------------------------------------------------------------------
+ * 3-D block layout (Sec. 3.3: visual tokens in non-overlapping (B_t, B_h, B_w)
+ * blocks; the fused Q-Prep, KV-Prep and Untile Scatter of its operator fusion).
+ *
+ * Linear (AR) order: keys are [n_text text tokens][T_ctx context frames][T_q chunk
+ * frames], queries are the T_q chunk frames; a frame is Hs x Ws tokens in raster
+ * order, token (t, y, x) of a run of frames at (t Hs + y) Ws + x.
+ * Blocks: the text in 1-D blocks of `block` tokens; each run of frames (context,
+ * chunk) in 3-D blocks of bt x bh x bw tokens, in raster order of their block
+ * coordinates, cut at the grid edges (fewer tokens there).  Inside a 3-D block,
+ * tokens are in raster order.
+ * Block-major (tiled) buffers give every block `block` slots: its tokens first, in
+ * the order above, then zero padding.  Key blocks: NT = ceil(n_text/block) text
+ * blocks, NC context blocks, NQ chunk blocks; query blocks: the NQ chunk blocks.
+ * The tiled problem is the la_shape written by la_grid3d_shape (Lq = NQ block,
+ * Lk = (NT + NC + NQ) block, n_text = NT block, frame_tokens = 0), so text and
+ * chunk blocks are forced and the NC context blocks are the historical candidates.
+ * The padding of key blocks is masked through the per-block valid counts
+ * (la_grid3d_valid, la_sparse_attn_fwd_valid); padded query rows are dropped by
+ * la_untile_o_3d.
+ * -------------------------------------------------------------------------- */
+typedef struct la_grid3d {
+  int32_t B, H, d;       /* batch, heads, head dimension (64 or 128) */
+  int32_t n_text;        /* text tokens (>= 0) */
+  int32_t T_ctx, T_q;    /* context frames (>= 0) and chunk frames (>= 1) */
+  int32_t Hs, Ws;        /* latent frame height and width in tokens (>= 1) */
+  int32_t bt, bh, bw;    /* 3-D block extents (>= 1), bt*bh*bw <= block */
+  int32_t block;         /* slots per block in the tiled buffers: 64 or 128 */
+} la_grid3d;
+
+/* Part bits of la_prep_kv_3d: which regions of the tiled K/V buffers to write. */
+enum { LA_PART_TEXT = 1, LA_PART_CONTEXT = 2, LA_PART_CHUNK = 4, LA_PART_ALL = 7 };
+
+/* Host-only.  Validates the grid and writes the la_shape of the tiled problem.
+ * LA_ERR_ARG for NULL pointers, LA_ERR_SHAPE for an invalid grid or a tiled shape
+ * la_shape does not accept. */
+la_status la_grid3d_shape(const la_grid3d* grid, la_shape* tiled);
+
+/* Host-only.  Valid tokens per block, into host arrays: qvalid int32 [NQ] (may be
+ * NULL) and kvalid int32 [NT + NC + NQ] (may be NULL). */
+la_status la_grid3d_valid(const la_grid3d* grid, int32_t* qvalid, int32_t* kvalid);
+
+/* Fused Q-Prep (Sec. 3.3, operator fusion; pooling equation): one pass over the
+ * chunk queries that writes them block-major and pools every query block.
+ *   q        bf16 [B, H, T_q Hs Ws, d], linear order                    (input)
+ *   q_tiled  bf16 [B, H, NQ block, d]: block-major, padding slots zero
+ *   qbar     float [B, H, NQ, d] or NULL: mean of each block's tokens (fp32 sums) */
+la_status la_prep_q_3d(const la_grid3d* grid, const void* q, void* q_tiled, float* qbar, void* stream);
+
+/* Fused KV-Prep (Sec. 3.3, operator fusion; pooling equation): reads K and V
+ * together, writes the regions named in `parts` of the block-major buffers and
+ * pools the K blocks it writes.  Regions not named are left untouched (a text or
+ * context region written once can be kept across calls).
+ *   k, v      bf16 [B, H, n_text + (T_ctx + T_q) Hs Ws, d], linear order   (inputs)
+ *   k_tiled, v_tiled  bf16 [B, H, (NT + NC + NQ) block, d]
+ *   kbar      float [B, H, NT + NC + NQ, d] or NULL: block means of K (rows of the
+ *             written regions only)
+ *   parts     non-zero subset of LA_PART_ALL, else LA_ERR_ARG. */
+la_status la_prep_kv_3d(const la_grid3d* grid, const void* k, const void* v, uint32_t parts,
+                        void* k_tiled, void* v_tiled, float* kbar, void* stream);
+
+/* Block selection from pooled means (Sec. 3.3, selection equation), for block
+ * layouts pooled elsewhere (la_prep_q_3d, la_prep_kv_3d).
+ *   shape  the tiled shape; qbar float [B, H, NQ, d], kbar float [B, H, NK, d] (rows
+ *          of the M historical blocks are read).
+ * Rules, outputs and errors as la_select_blocks / la_select_blocks_topk. */
+la_status la_select_pooled(const la_shape* shape, const float* qbar, const float* kbar, float tau,
+                           uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, size_t ws_bytes,
+                           void* stream);
+la_status la_select_pooled_topk(const la_shape* shape, const float* qbar, const float* kbar,
+                                int32_t keep_blocks, uint8_t* mask, int32_t* counts, int32_t* idx,
+                                void* ws, size_t ws_bytes, void* stream);
+
+/* la_sparse_attn_fwd / la_sparse_attn_plan for key blocks with padding.
+ *   kvalid  int32 [NK] device array: key block m holds valid keys at its first
+ *           kvalid[m] slots (clamped to [0, block]); the others are invisible.
+ *           NULL = every slot valid (the plain calls).
+ * la_sparse_attn_run and la_sparse_attn_merge serve both plans unchanged. */
+la_status la_sparse_attn_fwd_valid(const la_shape* shape, const void* q, const void* k, const void* v,
+                                   const int32_t* counts, const int32_t* idx, const int32_t* kvalid,
+                                   float scale, void* o, float* lse, void* ws, size_t ws_bytes,
+                                   void* stream);
+la_status la_sparse_attn_plan_valid(const la_shape* shape, const int32_t* counts, const int32_t* idx,
+                                    const int32_t* kvalid, void* ws, size_t ws_bytes, void* stream);
+
+/* Fused Untile Scatter (Sec. 3.3, operator fusion): block-major attention output back
+ * to linear order; padding slots are dropped.
+ *   o_tiled   bf16 [B, H, NQ block, d]; lse_tiled float [B, H, NQ block] or NULL (inputs)
+ *   o         bf16 [B, H, T_q Hs Ws, d]; lse float [B, H, T_q Hs Ws] (written when both
+ *             lse pointers are given) */
+la_status la_untile_o_3d(const la_grid3d* grid, const void* o_tiled, const float* lse_tiled, void* o,
+                         float* lse, void* stream);
+
 /* Static description of a status code. */
 const char* la_status_string(la_status status);
 

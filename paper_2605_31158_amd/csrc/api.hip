@@ -84,6 +84,32 @@ la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void
   return select_common(shape, q, k, 1.0f, keep_blocks, mask, counts, idx, ws, ws_bytes, stream);
 }
 
+static la_status select_pooled_common(const la_shape* shape, const float* qbar, const float* kbar, float tau,
+                                      int keep_fixed, uint8_t* mask, int32_t* counts, int32_t* idx, void* ws,
+                                      size_t ws_bytes, void* stream) {
+  Dims dm;
+  la_status st = make_dims(shape, &dm);
+  if (st != LA_OK) return st;
+  if (!qbar || !kbar || !counts || !idx) return LA_ERR_ARG;
+  if (misaligned(qbar) || misaligned(kbar)) return LA_ERR_ARG;
+  if (!ws || ws_bytes < select_ws_bytes(dm) || ((uintptr_t)ws & 255u)) return LA_ERR_WORKSPACE;
+  hipError_t e = launch_select_pooled(dm, qbar, kbar, tau, keep_fixed, mask, counts, idx, ws, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_select_pooled(const la_shape* shape, const float* qbar, const float* kbar, float tau, uint8_t* mask,
+                           int32_t* counts, int32_t* idx, void* ws, size_t ws_bytes, void* stream) {
+  if (!(tau > 0.0f)) return LA_ERR_ARG;
+  return select_pooled_common(shape, qbar, kbar, tau, -1, mask, counts, idx, ws, ws_bytes, stream);
+}
+
+la_status la_select_pooled_topk(const la_shape* shape, const float* qbar, const float* kbar, int32_t keep_blocks,
+                                uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, size_t ws_bytes,
+                                void* stream) {
+  if (keep_blocks < 0) return LA_ERR_ARG;
+  return select_pooled_common(shape, qbar, kbar, 1.0f, keep_blocks, mask, counts, idx, ws, ws_bytes, stream);
+}
+
 static la_status attn_check(const la_shape* shape, Dims* dm, void* ws, size_t ws_bytes) {
   la_status st = make_dims(shape, dm);
   if (st != LA_OK) return st;
@@ -102,29 +128,40 @@ static float effective_scale(float scale, const Dims& dm) {
   return scale > 0.0f ? scale : 1.0f / sqrtf((float)dm.d);
 }
 
-la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k, const void* v,
-                             const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
-                             void* ws, size_t ws_bytes, void* stream) {
+la_status la_sparse_attn_fwd_valid(const la_shape* shape, const void* q, const void* k, const void* v,
+                                   const int32_t* counts, const int32_t* idx, const int32_t* kvalid, float scale,
+                                   void* o, float* lse, void* ws, size_t ws_bytes, void* stream) {
   Dims dm;
   la_status st = attn_check(shape, &dm, ws, ws_bytes);
   if (st == LA_OK) st = qkvo_check(q, k, v, o, scale);
   if (st == LA_OK && (!counts || !idx)) st = LA_ERR_ARG;
   if (st != LA_OK) return st;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_attn_plan(dm, counts, idx, ws, s);
+  hipError_t e = launch_attn_plan(dm, counts, idx, kvalid, ws, s);
   if (e == hipSuccess) e = launch_attn_run(dm, q, k, v, effective_scale(scale, dm), o, lse, ws, s);
   if (e == hipSuccess) e = launch_attn_merge(dm, o, lse, ws, s);
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 
-la_status la_sparse_attn_plan(const la_shape* shape, const int32_t* counts, const int32_t* idx, void* ws,
-                              size_t ws_bytes, void* stream) {
+la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k, const void* v,
+                             const int32_t* counts, const int32_t* idx, float scale, void* o, float* lse,
+                             void* ws, size_t ws_bytes, void* stream) {
+  return la_sparse_attn_fwd_valid(shape, q, k, v, counts, idx, nullptr, scale, o, lse, ws, ws_bytes, stream);
+}
+
+la_status la_sparse_attn_plan_valid(const la_shape* shape, const int32_t* counts, const int32_t* idx,
+                                    const int32_t* kvalid, void* ws, size_t ws_bytes, void* stream) {
   Dims dm;
   la_status st = attn_check(shape, &dm, ws, ws_bytes);
   if (st != LA_OK) return st;
   if (!counts || !idx) return LA_ERR_ARG;
-  hipError_t e = launch_attn_plan(dm, counts, idx, ws, (hipStream_t)stream);
+  hipError_t e = launch_attn_plan(dm, counts, idx, kvalid, ws, (hipStream_t)stream);
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_sparse_attn_plan(const la_shape* shape, const int32_t* counts, const int32_t* idx, void* ws,
+                              size_t ws_bytes, void* stream) {
+  return la_sparse_attn_plan_valid(shape, counts, idx, nullptr, ws, ws_bytes, stream);
 }
 
 la_status la_sparse_attn_run(const la_shape* shape, const void* q, const void* k, const void* v, float scale,
@@ -154,6 +191,71 @@ la_status la_mask_to_list(const la_shape* shape, const uint8_t* mask, int32_t* c
   if (st != LA_OK) return st;
   if (!mask || !counts || !idx) return LA_ERR_ARG;
   hipError_t e = launch_mask_to_list(dm, mask, counts, idx, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_grid3d_shape(const la_grid3d* grid, la_shape* tiled) {
+  if (!tiled) return LA_ERR_ARG;
+  G3Dims gd;
+  la_status st = make_g3dims(grid, &gd);
+  if (st != LA_OK) return st;
+  *tiled = gd.shape;
+  return LA_OK;
+}
+
+la_status la_grid3d_valid(const la_grid3d* grid, int32_t* qvalid, int32_t* kvalid) {
+  G3Dims gd;
+  la_status st = make_g3dims(grid, &gd);
+  if (st != LA_OK) return st;
+  // tokens of 3-D block n of a run of T frames: the block's extents cut at the grid edges
+  auto count3 = [&](int T, int n) {
+    const int per_frame = gd.nby * gd.nbx;
+    const int ct = n / per_frame, rem = n % per_frame;
+    const int cy = rem / gd.nbx, cx = rem % gd.nbx;
+    const int et = T - ct * gd.bt < gd.bt ? T - ct * gd.bt : gd.bt;
+    const int ey = gd.Hs - cy * gd.bh < gd.bh ? gd.Hs - cy * gd.bh : gd.bh;
+    const int ex = gd.Ws - cx * gd.bw < gd.bw ? gd.Ws - cx * gd.bw : gd.bw;
+    return et * ey * ex;
+  };
+  if (qvalid)
+    for (int n = 0; n < gd.NQ; ++n) qvalid[n] = count3(gd.T_q, n);
+  if (kvalid) {
+    for (int n = 0; n < gd.NT; ++n) kvalid[n] = gd.n_text - n * gd.block < gd.block ? gd.n_text - n * gd.block : gd.block;
+    for (int n = 0; n < gd.NC; ++n) kvalid[gd.NT + n] = count3(gd.T_ctx, n);
+    for (int n = 0; n < gd.NQ; ++n) kvalid[gd.NT + gd.NC + n] = count3(gd.T_q, n);
+  }
+  return LA_OK;
+}
+
+la_status la_prep_q_3d(const la_grid3d* grid, const void* q, void* q_tiled, float* qbar, void* stream) {
+  G3Dims gd;
+  la_status st = make_g3dims(grid, &gd);
+  if (st != LA_OK) return st;
+  if (!q || !q_tiled || misaligned(q) || misaligned(q_tiled) || misaligned(qbar)) return LA_ERR_ARG;
+  hipError_t e = launch_prep_q(gd, q, q_tiled, qbar, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_prep_kv_3d(const la_grid3d* grid, const void* k, const void* v, uint32_t parts, void* k_tiled,
+                        void* v_tiled, float* kbar, void* stream) {
+  G3Dims gd;
+  la_status st = make_g3dims(grid, &gd);
+  if (st != LA_OK) return st;
+  if (parts == 0 || (parts & ~(uint32_t)LA_PART_ALL)) return LA_ERR_ARG;
+  if (!k || !v || !k_tiled || !v_tiled) return LA_ERR_ARG;
+  if (misaligned(k) || misaligned(v) || misaligned(k_tiled) || misaligned(v_tiled) || misaligned(kbar))
+    return LA_ERR_ARG;
+  hipError_t e = launch_prep_kv(gd, k, v, parts, k_tiled, v_tiled, kbar, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_untile_o_3d(const la_grid3d* grid, const void* o_tiled, const float* lse_tiled, void* o, float* lse,
+                         void* stream) {
+  G3Dims gd;
+  la_status st = make_g3dims(grid, &gd);
+  if (st != LA_OK) return st;
+  if (!o_tiled || !o || misaligned(o_tiled) || misaligned(o)) return LA_ERR_ARG;
+  hipError_t e = launch_untile_o(gd, o_tiled, lse_tiled, o, lse, (hipStream_t)stream);
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 

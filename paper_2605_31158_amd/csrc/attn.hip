@@ -58,6 +58,8 @@ constexpr int QR = 256;         // query rows per unit (workgroup)
 constexpr int kMaxPersist = 256;        // persistent workgroups: one per CU, at most 256
 // flags of a tile record (see TileRef)
 constexpr int kFlFrom0 = 1 << 4, kFlToEnd = 1 << 5, kFlFirst = 1 << 6, kFlLast = 1 << 7, kFlValid = 1 << 8;
+// Bits 16..22 of a tile record's flags: keys at the end of the tile that are padding (0..64).
+constexpr int kFlPadShift = 16;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
@@ -252,17 +254,19 @@ __device__ __forceinline__ void pv_tile(const unsigned char* __restrict__ vb, co
   __builtin_amdgcn_sched_group_barrier(kSgMfma, AHEAD, 0);
 }
 
-// Masks of one tile (ragged tail, frame-causal pairs): invisible keys get -inf.  Lane holds keys
-// key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row (column l%32); the two lanes l and
-// l^32 together hold the row's 64 keys.
-__device__ __forceinline__ void mask_tile(f32x16* sacc, int key0, const WaveCtx& w) {
-  if (key0 + KT > w.klimit_wave) {
+// Masks of one tile (ragged tail, frame-causal pairs, padding at the end of the tile): invisible
+// keys get -inf.  Lane holds keys key0 + 32 kt + 8 (i/4) + 4 (l/32) + i%4 of its query row
+// (column l%32); the two lanes l and l^32 together hold the row's 64 keys.
+__device__ __forceinline__ void mask_tile(f32x16* sacc, int key0, int fl, const WaveCtx& w) {
+  const int pad = (fl >> kFlPadShift) & 127;
+  if (key0 + KT > w.klimit_wave || pad) {
+    const int lim = min(w.klimit, key0 + KT - pad);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int key = key0 + 32 * kt + 8 * (i >> 2) + 4 * w.h + (i & 3);
-        if (key >= w.klimit) sacc[kt][i] = -INFINITY;
+        if (key >= lim) sacc[kt][i] = -INFINITY;
       }
   }
 }
@@ -456,9 +460,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t*
 
 // Expands unit u's union list into one record per 64-key tile at its place tstart[u] in the
 // global tile sequence, where tstart[u] = tiles of the units before u (summed here by the
-// workgroup); unit U-1 also writes tstart[U] = total.
+// workgroup); unit U-1 also writes tstart[U] = total.  With kvalid (valid keys at the front of
+// each key block), a tile's padding keys are counted into its flags.
 __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t* __restrict__ ulist,
-                                                                  const int32_t* __restrict__ ucount, int U, int NK,
+                                                                  const int32_t* __restrict__ ucount,
+                                                                  const int32_t* __restrict__ kvalid, int U, int NK,
                                                                   int block, int row_tiles, int4* __restrict__ trec,
                                                                   int32_t* __restrict__ tstart) {
   __shared__ int sh[kPlanThreads / 64];
@@ -486,8 +492,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t*
     int key0 = 0, bits = 0;
     if (nt > 0) {
       const int e = ul[nsub == 2 ? (a >> 1) : a];
-      key0 = (e >> 4) * block + (nsub == 2 ? (a & 1) * KT : 0);
+      const int sub = nsub == 2 ? (a & 1) : 0;
+      key0 = (e >> 4) * block + sub * KT;
       bits = e & 15;
+      if (kvalid) {
+        const int kv = min(max(kvalid[e >> 4], 0), block) - sub * KT;
+        bits |= (KT - min(max(kv, 0), KT)) << kFlPadShift;
+      }
     }
     out[a] = int4{key0, bh, u, bits | (a == 0 ? kFlFrom0 : 0) | (a == n - 1 ? kFlToEnd : 0)};
   }
@@ -660,7 +671,7 @@ __device__ __forceinline__ void m_phase(WaveState<D>& st, WaveCtx& w, int prev_f
 template <int D>
 __device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, const TileRef& cur, const KArgs& ka) {
   const bool use = cur.valid() && cur.owned(ka.my_list) && st.rows;
-  if (use) mask_tile(st.sacc, cur.key0, w);
+  if (use) mask_tile(st.sacc, cur.key0, cur.fl, w);
   softmax_tile<D>(st.sacc, st.pb, st.oacc, st.m_run, st.l_run, w.scale_log2, use);
 }
 
@@ -963,7 +974,8 @@ int persistent_workgroups() {
 
 size_t attn_ws_bytes(const Dims& dm) { return attn_ws_layout(dm, nullptr).bytes; }
 
-hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t* idx, void* ws, hipStream_t st) {
+hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t* idx, const int32_t* kvalid,
+                            void* ws, hipStream_t st) {
   const int row_tiles = ceil_div(dm.Lq, QR);
   const int U = dm.BH * row_tiles;
   AttnWs w = attn_ws_layout(dm, ws);
@@ -972,8 +984,8 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
                      idx, rows, dm.NK, dm.h0, dm.h1, w.keys);
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
                      st, counts, idx, w.keys, dm.NQ, dm.NK, dm.block, row_tiles, w.qmap, w.ulist, w.ucount);
-  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, U, dm.NK, dm.block,
-                     row_tiles, w.trec, w.tstart);
+  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U, dm.NK,
+                     dm.block, row_tiles, w.trec, w.tstart);
   return hipGetLastError();
 }
 

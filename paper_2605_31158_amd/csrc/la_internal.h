@@ -39,14 +39,36 @@ size_t attn_ws_bytes(const Dims& dm);
 // Launchers (defined next to their kernels); they only enqueue.
 hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau, int keep_fixed,
                          uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st);
+// Selection from pooled means given by the caller: qbar [BH, NQ, d], kbar [BH, NK, d].
+hipError_t launch_select_pooled(const Dims& dm, const float* qbar, const float* kbar, float tau, int keep_fixed,
+                                uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st);
 hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,
                                hipStream_t st);
 // The attention pass: work plan from the lists, the attention kernel over the plan, merge of
 // the units split across workgroups.
-hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t* idx, void* ws, hipStream_t st);
+// kvalid: valid keys at the front of each key block, or NULL (all valid).
+hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t* idx, const int32_t* kvalid,
+                            void* ws, hipStream_t st);
 hipError_t launch_attn_run(const Dims& dm, const void* q, const void* k, const void* v, float scale, void* o,
                            float* lse, void* ws, hipStream_t st);
 hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipStream_t st);
+
+// The 3-D block layout of a la_grid3d: block counts, linear lengths and the tiled la_shape.
+struct G3Dims {
+  int Hs, Ws, bt, bh, bw, nby, nbx;
+  int n_text, T_ctx, T_q, d, block, BH;
+  int NT, NC, NQ, NK;   // text, context and chunk blocks; NK = NT + NC + NQ
+  int F;                // tokens per frame
+  int Lq_lin, Lk_lin;   // tokens of the linear query and key sequences
+  la_shape shape;       // the tiled problem
+};
+// Validates the grid and fills G3Dims; LA_OK, LA_ERR_ARG or LA_ERR_SHAPE.
+la_status make_g3dims(const la_grid3d* g, G3Dims* out);
+hipError_t launch_prep_q(const G3Dims& gd, const void* q, void* q_tiled, float* qbar, hipStream_t st);
+hipError_t launch_prep_kv(const G3Dims& gd, const void* k, const void* v, uint32_t parts, void* k_tiled,
+                          void* v_tiled, float* kbar, hipStream_t st);
+hipError_t launch_untile_o(const G3Dims& gd, const void* o_tiled, const float* lse_tiled, void* o, float* lse,
+                           hipStream_t st);
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

@@ -100,10 +100,12 @@ __device__ inline f32x4 mfma_f32(float a, float b, f32x4 c) {
 
 constexpr int kScoreThreads = 512;   // 8 waves: one pooled block in flight per wave
 
-template <int D, int BLOCK, int GB>
-__global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const uint16_t* __restrict__ k,
+// POOLED: the key means come in as kbar fp32 [BH, NK, D] (pooled by the caller) instead of
+// being pooled here from k bf16 [BH, Lk, D].
+template <int D, int BLOCK, int GB, bool POOLED>
+__global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const void* __restrict__ kin,
                                                                 const float* __restrict__ qbar,
-                                                                float* __restrict__ scores, int Lk, int NQ,
+                                                                float* __restrict__ scores, int Lk, int NK, int NQ,
                                                                 int h0, int M, float inv_sqrt_d) {
   constexpr int LD = D + kPadF;
   __shared__ __attribute__((aligned(16))) float kb[GB][LD];
@@ -114,8 +116,16 @@ __global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const uint1
   const int gcount = min(GB, M - m0);
   constexpr int CH = D / 8;
   const float inv_block = 1.0f / (float)BLOCK;
+  const uint16_t* __restrict__ k = (const uint16_t*)kin;
+  const float* __restrict__ kbar = (const float*)kin;
   for (int g = wave; g < GB; g += kScoreThreads / 64) {
-    if (g < gcount) {
+    if (POOLED) {
+      if (lane < D / 4) {
+        f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (g < gcount) x = *(const f32x4*)(kbar + ((size_t)bh * NK + h0 + m0 + g) * D + lane * 4);
+        *(f32x4*)&kb[g][lane * 4] = x;
+      }
+    } else if (g < gcount) {
       const int j = h0 + m0 + g;   // historical blocks are whole: no ragged rows
       float a[8];
       wave_block_sum<D, BLOCK>(k + ((size_t)bh * Lk + (size_t)j * BLOCK) * D, BLOCK, a);
@@ -419,32 +429,32 @@ __global__ __launch_bounds__(kThreads) void mask_to_list_kernel(const uint8_t* _
   if (lane == 0) counts[row] = pos;
 }
 
-template <int D, int BLOCK>
-void launch_pools(const Dims& dm, const void* q, const void* k, float* qbar, float* scores, hipStream_t st) {
+// Scores of the pooled keys (pooled here from k, or given as kbar when POOLED) against qbar.
+template <int D, int BLOCK, bool POOLED>
+void launch_score(const Dims& dm, const void* kin, const float* qbar, float* scores, hipStream_t st) {
   const float inv_sqrt_d = 1.0f / sqrtf((float)dm.d);
-  hipLaunchKernelGGL((pool_q_kernel<D, BLOCK>), dim3(ceil_div(dm.NQ, kThreads / 64), dm.BH), dim3(kThreads), 0,
-                     st, (const uint16_t*)q, qbar, dm.Lq, dm.NQ);
   // 32 key blocks per workgroup when that still gives >= 1 workgroup per CU, else 16
   if ((int64_t)ceil_div(dm.M, 32) * dm.BH >= 256)
-    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 32>), dim3(ceil_div(dm.M, 32), dm.BH), dim3(kScoreThreads),
-                       0, st, (const uint16_t*)k, qbar, scores, dm.Lk, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
+    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 32, POOLED>), dim3(ceil_div(dm.M, 32), dm.BH),
+                       dim3(kScoreThreads), 0, st, kin, qbar, scores, dm.Lk, dm.NK, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
   else
-    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 16>), dim3(ceil_div(dm.M, 16), dm.BH), dim3(kScoreThreads),
-                       0, st, (const uint16_t*)k, qbar, scores, dm.Lk, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
+    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 16, POOLED>), dim3(ceil_div(dm.M, 16), dm.BH),
+                       dim3(kScoreThreads), 0, st, kin, qbar, scores, dm.Lk, dm.NK, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
 }
 
-}  // namespace
+template <int D, int BLOCK>
+void launch_pools(const Dims& dm, const void* q, const void* k, float* qbar, float* scores, hipStream_t st) {
+  hipLaunchKernelGGL((pool_q_kernel<D, BLOCK>), dim3(ceil_div(dm.NQ, kThreads / 64), dm.BH), dim3(kThreads), 0,
+                     st, (const uint16_t*)q, qbar, dm.Lq, dm.NQ);
+  launch_score<D, BLOCK, false>(dm, k, qbar, scores, st);
+}
 
-hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau, int keep_fixed,
-                         uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st) {
-  float* qbar = (float*)ws;
-  float* scores = (float*)((char*)ws + align256((size_t)dm.BH * dm.NQ * dm.d * sizeof(float)));
-  if (dm.M > 0) {
-    if (dm.d == 128 && dm.block == 64) launch_pools<128, 64>(dm, q, k, qbar, scores, st);
-    else if (dm.d == 128) launch_pools<128, 128>(dm, q, k, qbar, scores, st);
-    else if (dm.block == 64) launch_pools<64, 64>(dm, q, k, qbar, scores, st);
-    else launch_pools<64, 128>(dm, q, k, qbar, scores, st);
-  }
+float* scores_ws(const Dims& dm, void* ws) {
+  return (float*)((char*)ws + align256((size_t)dm.BH * dm.NQ * dm.d * sizeof(float)));
+}
+
+hipError_t launch_rows(const Dims& dm, const float* scores, float tau, int keep_fixed, uint8_t* mask,
+                       int32_t* counts, int32_t* idx, hipStream_t st) {
   const dim3 grid(ceil_div(dm.NQ, kThreads / 64), dm.BH);
 #define LA_SELECT(NPER)                                                                                      \
   hipLaunchKernelGGL(select_rows_kernel<NPER>, grid, dim3(kThreads), 0, st, scores, dm.NQ, dm.NK, dm.M, dm.h0, \
@@ -455,6 +465,31 @@ hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau
   else LA_SELECT(64);
 #undef LA_SELECT
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau, int keep_fixed,
+                         uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st) {
+  float* qbar = (float*)ws;
+  float* scores = scores_ws(dm, ws);
+  if (dm.M > 0) {
+    if (dm.d == 128 && dm.block == 64) launch_pools<128, 64>(dm, q, k, qbar, scores, st);
+    else if (dm.d == 128) launch_pools<128, 128>(dm, q, k, qbar, scores, st);
+    else if (dm.block == 64) launch_pools<64, 64>(dm, q, k, qbar, scores, st);
+    else launch_pools<64, 128>(dm, q, k, qbar, scores, st);
+  }
+  return launch_rows(dm, scores, tau, keep_fixed, mask, counts, idx, st);
+}
+
+hipError_t launch_select_pooled(const Dims& dm, const float* qbar, const float* kbar, float tau, int keep_fixed,
+                                uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st) {
+  float* scores = scores_ws(dm, ws);
+  if (dm.M > 0) {
+    if (dm.d == 128) launch_score<128, 64, true>(dm, kbar, qbar, scores, st);
+    else launch_score<64, 64, true>(dm, kbar, qbar, scores, st);
+  }
+  return launch_rows(dm, scores, tau, keep_fixed, mask, counts, idx, st);
 }
 
 hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,

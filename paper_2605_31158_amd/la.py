@@ -34,9 +34,21 @@ class LaError(RuntimeError):
         self.status = status
 
 
+class Grid3D(ctypes.Structure):
+    """la_grid3d: 3-D block layout of one AR chunk (text, context frames, chunk frames)."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "H", "d", "n_text", "T_ctx", "T_q", "Hs", "Ws", "bt", "bh", "bw",
+                                              "block")]
+
+    def __repr__(self):
+        return "Grid3D(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
+
+
+LA_PART_TEXT, LA_PART_CONTEXT, LA_PART_CHUNK, LA_PART_ALL = 1, 2, 4, 7
+
 _lib = None
 _P = ctypes.c_void_p
 _SP = ctypes.POINTER(Shape)
+_GP = ctypes.POINTER(Grid3D)
 
 _SIGNATURES = {
     "la_workspace_bytes": (ctypes.c_size_t, [_SP]),
@@ -47,6 +59,16 @@ _SIGNATURES = {
     "la_sparse_attn_run": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_merge": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_mask_to_list": (ctypes.c_int, [_SP, _P, _P, _P, _P]),
+    "la_grid3d_shape": (ctypes.c_int, [_GP, _SP]),
+    "la_grid3d_valid": (ctypes.c_int, [_GP, _P, _P]),
+    "la_prep_q_3d": (ctypes.c_int, [_GP, _P, _P, _P, _P]),
+    "la_prep_kv_3d": (ctypes.c_int, [_GP, _P, _P, ctypes.c_uint32, _P, _P, _P, _P]),
+    "la_select_pooled": (ctypes.c_int, [_SP, _P, _P, ctypes.c_float, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_select_pooled_topk": (ctypes.c_int, [_SP, _P, _P, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_sparse_attn_fwd_valid": (ctypes.c_int, [_SP, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P,
+                                                ctypes.c_size_t, _P]),
+    "la_sparse_attn_plan_valid": (ctypes.c_int, [_SP, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_untile_o_3d": (ctypes.c_int, [_GP, _P, _P, _P, _P, _P]),
     "la_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "la_abi_version": (ctypes.c_int32, []),
 }
@@ -154,8 +176,11 @@ def _select(fn, rule_arg, q, k, block, n_text, want_mask, ws, out):
 def sparse_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, counts: torch.Tensor,
                     idx: torch.Tensor, block: int, scale: Optional[float] = None, n_text: int = 0,
                     frame_tokens: int = 0, want_lse: bool = False, ws: Optional[torch.Tensor] = None,
-                    out: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None):
-    """Block-sparse attention over the kept lists -> o bf16 [B,H,Lq,d] (and lse fp32 [B,H,Lq])."""
+                    out: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None,
+                    kvalid: Optional[torch.Tensor] = None):
+    """Block-sparse attention over the kept lists -> o bf16 [B,H,Lq,d] (and lse fp32 [B,H,Lq]).
+    kvalid (int32 [NK] on the GPU): valid keys at the front of each key block
+    (la_sparse_attn_fwd_valid); the other slots are padding."""
     _check_qkv("q", q)
     B, H, Lq, d = q.shape
     _check_qkv("k", k, B, H, d)
@@ -173,9 +198,15 @@ def sparse_attn_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, counts: t
     lse = lse_out if lse_out is not None else (
         torch.empty((B, H, Lq), dtype=torch.float32, device=q.device) if want_lse else None)
     ws, nbytes = _workspace(shape, q.device, ws)
-    _call("la_sparse_attn_fwd", ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(counts), _ptr(idx),
-          ctypes.c_float(scale if scale is not None else 0.0), _ptr(o), _ptr(lse), _ptr(ws),
-          ctypes.c_size_t(nbytes), _stream(q))
+    sc = ctypes.c_float(scale if scale is not None else 0.0)
+    if kvalid is None:
+        _call("la_sparse_attn_fwd", ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(counts), _ptr(idx), sc,
+              _ptr(o), _ptr(lse), _ptr(ws), ctypes.c_size_t(nbytes), _stream(q))
+    else:
+        if kvalid.device != q.device or kvalid.dtype != torch.int32 or tuple(kvalid.shape) != (NK,):
+            raise ValueError(f"kvalid must be an int32 [{NK}] tensor on {q.device}")
+        _call("la_sparse_attn_fwd_valid", ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(counts), _ptr(idx),
+              _ptr(kvalid), sc, _ptr(o), _ptr(lse), _ptr(ws), ctypes.c_size_t(nbytes), _stream(q))
     return (o, lse) if (want_lse or lse_out is not None) else o
 
 
@@ -242,6 +273,130 @@ def mask_to_list(mask: torch.Tensor, block: int, Lq: int, Lk: int, d: int = 128)
     idx = torch.empty((B, H, NQ, NK), dtype=torch.int32, device=mask.device)
     _call("la_mask_to_list", ctypes.byref(shape), _ptr(mask), _ptr(counts), _ptr(idx), _stream(mask))
     return counts, idx
+
+
+# ----------------------------------------------------------------------------------------------
+# 3-D block layout
+
+def grid3d(B, H, d, n_text, T_ctx, T_q, Hs, Ws, bt, bh, bw, block=128) -> Grid3D:
+    return Grid3D(B, H, d, n_text, T_ctx, T_q, Hs, Ws, bt, bh, bw, block)
+
+
+def grid3d_shape(g: Grid3D) -> Shape:
+    """la_shape of the tiled problem (Lq = NQ block, Lk = NK block, n_text = NT block)."""
+    shape = Shape()
+    _call("la_grid3d_shape", ctypes.byref(g), ctypes.byref(shape))
+    return shape
+
+
+def grid3d_valid(g: Grid3D):
+    """(qvalid int32 [NQ], kvalid int32 [NK]) as numpy arrays: valid tokens per block."""
+    import numpy as np
+    shape = grid3d_shape(g)
+    qv = np.zeros(nblocks(shape.Lq, g.block), dtype=np.int32)
+    kv = np.zeros(nblocks(shape.Lk, g.block), dtype=np.int32)
+    _call("la_grid3d_valid", ctypes.byref(g), qv.ctypes.data_as(_P), kv.ctypes.data_as(_P))
+    return qv, kv
+
+
+def _check_lin(name, t, g: Grid3D, L):
+    _check_qkv(name, t, g.B, g.H, g.d)
+    if t.shape[2] != L:
+        raise ValueError(f"{name} must hold {L} tokens, got {t.shape[2]}")
+
+
+def prep_q_3d(g: Grid3D, q: torch.Tensor, q_tiled: Optional[torch.Tensor] = None,
+              qbar: Optional[torch.Tensor] = None, want_qbar: bool = True):
+    """Fused Q-Prep: q linear [B,H,T_q Hs Ws,d] -> (q_tiled bf16 [B,H,NQ block,d], qbar fp32 [B,H,NQ,d])."""
+    _check_lin("q", q, g, g.T_q * g.Hs * g.Ws)
+    shape = grid3d_shape(g)
+    NQ = nblocks(shape.Lq, g.block)
+    if q_tiled is None:
+        q_tiled = torch.empty((g.B, g.H, shape.Lq, g.d), dtype=torch.bfloat16, device=q.device)
+    if qbar is None and want_qbar:
+        qbar = torch.empty((g.B, g.H, NQ, g.d), dtype=torch.float32, device=q.device)
+    _call("la_prep_q_3d", ctypes.byref(g), _ptr(q), _ptr(q_tiled), _ptr(qbar), _stream(q))
+    return q_tiled, qbar
+
+
+def prep_kv_3d(g: Grid3D, k: torch.Tensor, v: torch.Tensor, parts: int = LA_PART_ALL,
+               k_tiled: Optional[torch.Tensor] = None, v_tiled: Optional[torch.Tensor] = None,
+               kbar: Optional[torch.Tensor] = None, want_kbar: bool = True):
+    """Fused KV-Prep of the regions in `parts`: k, v linear [B,H,n_text+(T_ctx+T_q) Hs Ws,d] ->
+    (k_tiled, v_tiled bf16 [B,H,NK block,d], kbar fp32 [B,H,NK,d])."""
+    L = g.n_text + (g.T_ctx + g.T_q) * g.Hs * g.Ws
+    _check_lin("k", k, g, L)
+    _check_lin("v", v, g, L)
+    shape = grid3d_shape(g)
+    NK = nblocks(shape.Lk, g.block)
+    if k_tiled is None:
+        k_tiled = torch.empty((g.B, g.H, shape.Lk, g.d), dtype=torch.bfloat16, device=k.device)
+    if v_tiled is None:
+        v_tiled = torch.empty((g.B, g.H, shape.Lk, g.d), dtype=torch.bfloat16, device=k.device)
+    if kbar is None and want_kbar:
+        kbar = torch.empty((g.B, g.H, NK, g.d), dtype=torch.float32, device=k.device)
+    _call("la_prep_kv_3d", ctypes.byref(g), _ptr(k), _ptr(v), ctypes.c_uint32(parts), _ptr(k_tiled), _ptr(v_tiled),
+          _ptr(kbar), _stream(k))
+    return k_tiled, v_tiled, kbar
+
+
+def select_pooled(shape: Shape, qbar: torch.Tensor, kbar: torch.Tensor, tau: Optional[float] = None,
+                  keep_blocks: Optional[int] = None, want_mask: bool = True, ws: Optional[torch.Tensor] = None):
+    """Selection from pooled means (qbar fp32 [B,H,NQ,d], kbar fp32 [B,H,NK,d]) with the tau rule or
+    the top-keep_blocks rule -> (mask, counts, idx) as select_blocks."""
+    if (tau is None) == (keep_blocks is None):
+        raise ValueError("give exactly one of tau and keep_blocks")
+    B, H, d, block = shape.B, shape.H, shape.d, shape.block
+    NQ, NK = nblocks(shape.Lq, block), nblocks(shape.Lk, block)
+    for name, t, n in (("qbar", qbar, NQ), ("kbar", kbar, NK)):
+        if t.device.type != "cuda" or t.dtype != torch.float32 or tuple(t.shape) != (B, H, n, d) \
+                or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 {(B, H, n, d)} GPU tensor")
+    mask = torch.empty((B, H, NQ, NK), dtype=torch.uint8, device=qbar.device) if want_mask else None
+    counts = torch.empty((B, H, NQ), dtype=torch.int32, device=qbar.device)
+    idx = torch.empty((B, H, NQ, NK), dtype=torch.int32, device=qbar.device)
+    ws, nbytes = _workspace(shape, qbar.device, ws)
+    if tau is not None:
+        fn, arg = "la_select_pooled", ctypes.c_float(tau)
+    else:
+        fn, arg = "la_select_pooled_topk", ctypes.c_int32(keep_blocks)
+    _call(fn, ctypes.byref(shape), _ptr(qbar), _ptr(kbar), arg, _ptr(mask), _ptr(counts), _ptr(idx), _ptr(ws),
+          ctypes.c_size_t(nbytes), _stream(qbar))
+    return mask, counts, idx
+
+
+def untile_o_3d(g: Grid3D, o_tiled: torch.Tensor, lse_tiled: Optional[torch.Tensor] = None,
+                o: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None):
+    """Fused Untile Scatter: o_tiled [B,H,NQ block,d] (and lse_tiled) -> o linear [B,H,T_q Hs Ws,d] (and lse)."""
+    shape = grid3d_shape(g)
+    _check_lin("o_tiled", o_tiled, g, shape.Lq)
+    L = g.T_q * g.Hs * g.Ws
+    if o is None:
+        o = torch.empty((g.B, g.H, L, g.d), dtype=torch.bfloat16, device=o_tiled.device)
+    if lse is None and lse_tiled is not None:
+        lse = torch.empty((g.B, g.H, L), dtype=torch.float32, device=o_tiled.device)
+    _call("la_untile_o_3d", ctypes.byref(g), _ptr(o_tiled), _ptr(lse_tiled), _ptr(o), _ptr(lse), _stream(o_tiled))
+    return o, lse
+
+
+def sparse_attn_3d(g: Grid3D, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, tau: Optional[float] = None,
+                   keep_blocks: Optional[int] = None, scale: Optional[float] = None, want_lse: bool = False,
+                   kvalid: Optional[torch.Tensor] = None):
+    """The whole 3-D path on linear-order inputs: Q-Prep, KV-Prep, selection from the pooled means,
+    attention over the tiled buffers with the padding masked, Untile Scatter.  Returns
+    (o linear, lse linear or None, mask over the tiled blocks, counts, idx)."""
+    shape = grid3d_shape(g)
+    if kvalid is None:
+        kvalid = torch.from_numpy(grid3d_valid(g)[1]).to(q.device)
+    q_t, qbar = prep_q_3d(g, q)
+    k_t, v_t, kbar = prep_kv_3d(g, k, v)
+    ws, _ = _workspace(shape, q.device, None)
+    mask, counts, idx = select_pooled(shape, qbar, kbar, tau=tau, keep_blocks=keep_blocks, ws=ws)
+    res = sparse_attn_fwd(q_t, k_t, v_t, counts, idx, g.block, scale=scale, n_text=shape.n_text, want_lse=want_lse,
+                          ws=ws, kvalid=kvalid)
+    o_t, lse_t = res if want_lse else (res, None)
+    o, lse = untile_o_3d(g, o_t, lse_t)
+    return o, lse, mask, counts, idx
 
 
 def bf16_from_bits(bits, device="cuda") -> torch.Tensor:

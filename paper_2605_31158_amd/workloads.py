@@ -25,7 +25,7 @@ from typing import Dict, Optional
 import numpy as np
 
 __all__ = ["Workload", "WORKLOADS", "make_inputs", "make_clustered", "f32_to_bf16_bits",
-           "frame_slot_tables_size"]
+           "frame_slot_tables_size", "Workload3D", "WORKLOADS_3D", "make_inputs_3d"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -266,4 +266,125 @@ def make_clustered(B: int, H: int, Lq: int, Lk: int, d: int, block: int, seed: i
             else:
                 raise ValueError(v_kind)
             v[bi, hi] = f32_to_bf16_bits(vn)
+    return {"q": q, "k": k, "v": v}
+
+
+# ------------------------------------------------------------------------------------------------
+# 3-D block layout workloads (Sec. 3.3; block extents of the evaluated models: (4, 8, 4) on the
+# 30x52 latent grid, (4, 4, 8) on the 45x80 grid, 128 tokens per block)
+
+@dataclasses.dataclass(frozen=True)
+class Workload3D:
+    """One AR chunk in linear order: n_text text keys, T_ctx context frames, T_q chunk frames of
+    Hs x Ws tokens; blocks of bt x bh x bw tokens in `block` slots.  Context structure: the last
+    `window` context frames walk into the chunk frames (step 0.2); `n_related` of the earlier
+    frames copy a chunk frame's field; the other earlier frames are unrelated."""
+    name: str
+    B: int
+    H: int
+    d: int
+    n_text: int
+    T_ctx: int
+    T_q: int
+    Hs: int
+    Ws: int
+    bt: int
+    bh: int
+    bw: int
+    block: int
+    seed: int
+    window: int
+    n_related: int
+    tau: Optional[float] = None       # cumulative-mass rule, or
+    topk_r: Optional[float] = None    # the Top-floor(rM) rule with retained fraction r
+
+    @property
+    def frame_tokens(self) -> int:
+        return self.Hs * self.Ws
+
+    @property
+    def Lq(self) -> int:
+        return self.T_q * self.frame_tokens
+
+    @property
+    def Lk(self) -> int:
+        return self.n_text + (self.T_ctx + self.T_q) * self.frame_tokens
+
+    def replace(self, **kw) -> "Workload3D":
+        return dataclasses.replace(self, **kw)
+
+
+WORKLOADS_3D: Dict[str, Workload3D] = {
+    # ragged everywhere: 24-token blocks in 64 slots, frames and text not block multiples
+    "tiny_3d": Workload3D("tiny_3d", 1, 2, 64, 40, 6, 3, 7, 10, 2, 3, 4, 64, 10, 2, 1, tau=0.9),
+    # 480P latents (30x52), (4, 8, 4) blocks: 16 memory frames (3 related) + 8 window frames; the
+    # retained fraction 17.5% of the evaluated 480P model
+    "480p_3d": Workload3D("480p_3d", 1, 16, 128, 300, 24, 4, 30, 52, 4, 8, 4, 128, 11, 8, 3, topk_r=0.175),
+    # 720P latents (45x80), (4, 4, 8) blocks: 12 unrelated + 4 window frames
+    "720p_3d": Workload3D("720p_3d", 1, 24, 128, 0, 16, 4, 45, 80, 4, 4, 8, 128, 12, 4, 0, topk_r=0.175),
+}
+
+
+def _region_fields(wl: Workload3D, rng: np.random.Generator) -> np.ndarray:
+    """Centroid fields [T_ctx + T_q, ceil(Hs/bh), ceil(Ws/bw), d] (float32) for one head: one
+    centroid per region of bh x bw tokens of a frame."""
+    ry, rx = -(-wl.Hs // wl.bh), -(-wl.Ws // wl.bw)
+    std = lambda *shape: rng.standard_normal(shape, dtype=np.float32)
+    n_walk = min(wl.window, wl.T_ctx) + wl.T_q
+    walk = np.empty((n_walk, ry, rx, wl.d), np.float32)
+    walk[0] = std(ry, rx, wl.d)
+    for f in range(1, n_walk):
+        walk[f] = walk[f - 1] + np.float32(0.2) * std(ry, rx, wl.d)
+    n_early = wl.T_ctx - min(wl.window, wl.T_ctx)
+    early = std(n_early, ry, rx, wl.d)
+    if n_early > 0 and wl.n_related > 0:
+        rel = rng.choice(n_early, size=min(wl.n_related, n_early), replace=False)
+        src = rng.integers(0, wl.T_q, size=rel.size)
+        for m, c in zip(rel, src):
+            early[m] = walk[n_walk - wl.T_q + c]
+    return np.concatenate([early, walk], axis=0)
+
+
+def make_inputs_3d(wl: Workload3D, threads: int = 8) -> Dict[str, np.ndarray]:
+    """Draw q, k, v (bf16 bit patterns, linear order [B, H, L, d]) for a 3-D workload.
+
+    Recipe, per (batch, head) pair, from its own child of SeedSequence(seed):
+      1. centroid fields (`_region_fields`), one centroid per bh x bw region of each frame;
+      2. keys: text k_n ~ N(0, I_d); visual k = centroid(frame, region) + 0.5 * N(0, I_d);
+      3. queries (chunk frames): centroid(frame, region) + 0.5 * N(0, I_d);
+      4. values: v_n ~ N(0, I_d), independent of everything else.
+    Float32 arithmetic, then round-to-nearest-even to bfloat16.
+    """
+    B, H, d, F = wl.B, wl.H, wl.d, wl.frame_tokens
+    q = np.empty((B, H, wl.Lq, d), np.uint16)
+    k = np.empty((B, H, wl.Lk, d), np.uint16)
+    v = np.empty((B, H, wl.Lk, d), np.uint16)
+    seeds = np.random.SeedSequence(wl.seed).spawn(B * H)
+    ys, xs = np.divmod(np.arange(F), wl.Ws)
+    reg_y, reg_x = ys // wl.bh, xs // wl.bw
+    nf = wl.T_ctx + wl.T_q
+
+    def one(bh: int):
+        bi, hi = divmod(bh, H)
+        rng = np.random.default_rng(seeds[bh])
+        fields = _region_fields(wl, rng)
+        cent = fields[:, reg_y, reg_x, :].reshape(nf * F, d)
+        kn = rng.standard_normal((wl.Lk, d), dtype=np.float32)
+        kn *= np.float32(0.5)
+        kn[wl.n_text:] += cent
+        kn[:wl.n_text] *= np.float32(2.0)
+        k[bi, hi] = f32_to_bf16_bits(kn)
+        del kn
+        qn = rng.standard_normal((wl.Lq, d), dtype=np.float32)
+        qn *= np.float32(0.5)
+        qn += cent[wl.T_ctx * F:]
+        q[bi, hi] = f32_to_bf16_bits(qn)
+        v[bi, hi] = f32_to_bf16_bits(rng.standard_normal((wl.Lk, d), dtype=np.float32))
+
+    if threads > 1 and B * H > 1:
+        with ThreadPoolExecutor(min(threads, B * H)) as ex:
+            list(ex.map(one, range(B * H)))
+    else:
+        for bh in range(B * H):
+            one(bh)
     return {"q": q, "k": k, "v": v}
