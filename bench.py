@@ -8,6 +8,9 @@ entry point so that HIP events on the launch stream time every stage.  Prints ON
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
+NAME may also be a 3-D block workload (480p_3d, 720p_3d, tiny_3d): then a step is the 3-D path
+(Q-Prep, KV-Prep, selection from the pooled means, attention, Untile Scatter).
+
 value = kept-block TFLOP/s of the whole step (kept FLOPs / step time).  The line also
 carries the per-kernel split, the dense baseline (same attention kernel, every block
 kept), the roofline of the attention kernel (la_sparse_attn_run launches exactly that one
@@ -136,6 +139,204 @@ def cpu_baseline(wl, inp, mask_np, target_s: float):
                       f"affinity={len(os.sched_getaffinity(0))}"}
 
 
+def kept_flop_count_3d(mask_np, qvalid, kvalid, d: int) -> int:
+    """kept_flop_count for blocks with padding: 4 d x (valid query tokens of the block) x (valid
+    keys of the kept key blocks), summed over the kept (query block, key block) pairs."""
+    NQ, NK = mask_np.shape[-2], mask_np.shape[-1]
+    kept = mask_np.reshape(-1, NQ, NK).astype(np.int64)
+    q = np.asarray(qvalid, np.int64)
+    k = np.asarray(kvalid, np.int64)
+    return int(4 * d * (kept * q[:, None] * k[None, :]).sum())
+
+
+def prep_bytes_3d(wl, which: str) -> int:
+    """Algorithmic HBM bytes of one prep launch set: the valid tokens read once, every block-major
+    slot written once (bf16), the block means written (fp32).  which: "q", "kv" or "kv_chunk"."""
+    BH, d, blk = wl.B * wl.H, wl.d, wl.block
+    per_frame = -(-wl.Hs // wl.bh) * -(-wl.Ws // wl.bw)
+    NQ = -(-wl.T_q // wl.bt) * per_frame
+    NC = -(-wl.T_ctx // wl.bt) * per_frame
+    NT = -(-wl.n_text // blk)
+    if which == "q":
+        return BH * (wl.Lq * d * 2 + NQ * blk * d * 2 + NQ * d * 4)
+    if which == "kv":
+        return BH * (2 * wl.Lk * d * 2 + 2 * (NT + NC + NQ) * blk * d * 2 + (NT + NC + NQ) * d * 4)
+    return BH * (2 * wl.Lq * d * 2 + 2 * NQ * blk * d * 2 + NQ * d * 4)
+
+
+def cpu_baseline_3d(wl, inp, mask_np, qvalid, kvalid, target_s: float):
+    """The fp64 oracle on the host for the 3-D layout, head after head (selection of the head over
+    the block sets, then fp64 attention of its query blocks on the GPU's mask) until about
+    target_s seconds have passed; rate in kept TFLOP/s (valid tokens) over the heads done."""
+    from oracle import la_oracle as O
+    L = O.layout_3d(wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, wl.block)
+    rule = dict(tau=wl.tau) if wl.tau is not None else dict(topk_r=wl.topk_r)
+    flops = heads = blocks = 0
+    t0 = time.perf_counter()
+    NQ = len(L["qsets"])
+    while time.perf_counter() - t0 <= target_s:
+        for b in range(wl.B):
+            for h in range(wl.H):
+                O.select_blocks_sets(inp["q"][b:b + 1, h:h + 1], inp["k"][b:b + 1, h:h + 1], L["qsets"], L["ksets"],
+                                     L["forced"], **rule)
+                rows = [(b, h, i) for i in range(NQ)]
+                O.attention_sets_rows(inp["q"], inp["k"], inp["v"], L["qsets"], L["ksets"], mask_np, rows)
+                flops += kept_flop_count_3d(mask_np[b:b + 1, h:h + 1], qvalid, kvalid, wl.d)
+                blocks += NQ
+                heads += 1
+                if time.perf_counter() - t0 > target_s:
+                    break
+            if time.perf_counter() - t0 > target_s:
+                break
+    t_total = time.perf_counter() - t0
+    threads = None
+    try:
+        import threadpoolctl
+        threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
+    except Exception:
+        pass
+    return {"value": round(flops / t_total / 1e12, 5), "unit": "TFLOP/s", "cores": threads or os.cpu_count(),
+            "kind": "oracle",
+            "sample": f"{heads} heads of {wl.name}: fp64 selection of each head over the 3-D block sets and fp64 "
+                      f"attention of its {NQ} query blocks on the GPU's mask; {flops / 1e9:.1f} GFLOP kept in "
+                      f"{t_total:.1f} s; os.cpu_count()={os.cpu_count()}, affinity={len(os.sched_getaffinity(0))}"}
+
+
+def main_3d(args, wl):
+    """The 3-D block path: Q-Prep, KV-Prep, selection from the pooled means, attention (plan, run,
+    merge) over the block-major buffers, Untile Scatter; each stage timed with HIP events."""
+    import torch
+    from paper_2605_31158_amd import la
+    from paper_2605_31158_amd.workloads import make_inputs_3d
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    inp = make_inputs_3d(wl)
+    g = {x: la.bf16_from_bits(inp[x], dev) for x in "qkv"}
+    t_gen = time.perf_counter() - t_gen
+    B, H, d, blk = wl.B, wl.H, wl.d, wl.block
+    grid = la.grid3d(B, H, d, wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, blk)
+    shape = la.grid3d_shape(grid)
+    qv, kv = la.grid3d_valid(grid)
+    NQ, NK = shape.Lq // blk, shape.Lk // blk
+    M = (shape.Lk - shape.Lq - shape.n_text) // blk
+    keep_blocks = None if wl.tau is not None else int(math.floor(wl.topk_r * M))
+    ws = torch.empty(max(la.workspace_bytes(shape), 256), dtype=torch.uint8, device=dev)
+    q_t = torch.empty((B, H, shape.Lq, d), dtype=torch.bfloat16, device=dev)
+    k_t = torch.empty((B, H, shape.Lk, d), dtype=torch.bfloat16, device=dev)
+    v_t = torch.empty_like(k_t)
+    qbar = torch.empty((B, H, NQ, d), dtype=torch.float32, device=dev)
+    kbar = torch.empty((B, H, NK, d), dtype=torch.float32, device=dev)
+    mask = torch.empty((B, H, NQ, NK), dtype=torch.uint8, device=dev)
+    counts = torch.empty((B, H, NQ), dtype=torch.int32, device=dev)
+    idx = torch.empty((B, H, NQ, NK), dtype=torch.int32, device=dev)
+    kvalid = torch.from_numpy(kv).to(dev)
+    o_t = torch.empty_like(q_t)
+    o = torch.empty_like(g["q"])
+    stream = torch.cuda.current_stream(dev)
+    stages = la.bind_3d(grid, g["q"], g["k"], g["v"], q_t, k_t, v_t, qbar, kbar, mask, counts, idx, kvalid, o_t,
+                        None, o, None, ws, tau=wl.tau, keep_blocks=keep_blocks)
+    names = ("prep_q", "prep_kv", "select", "attn_plan", "attn_run", "attn_merge", "untile")
+    for _ in range(args.warmup):
+        for f in stages:
+            f()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(K)]
+    t0 = time.perf_counter()
+    for it in range(K):
+        ev[it][0].record(stream)
+        for j, f in enumerate(stages):
+            f()
+            ev[it][j + 1].record(stream)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / K
+    st_ms = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(len(stages))] for i in range(K)])
+    t = {n: float(np.mean(st_ms[:, j])) for j, n in enumerate(names)}
+
+    mask_np = mask.cpu().numpy()
+    kept_flops = float(kept_flop_count_3d(mask_np, qv, kv, d))
+    dense_flops = float(kept_flop_count_3d(np.ones_like(mask_np), qv, kv, d))
+    rho = kept_flops / dense_flops
+
+    def time_calls(calls, n):
+        for _ in range(2):
+            for f in calls:
+                f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            for f in calls:
+                f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    # the chunk's K/V only (text and context regions kept from an earlier call)
+    chunk_kv = la.bind_3d(grid, g["q"], g["k"], g["v"], q_t, k_t, v_t, qbar, kbar, mask, counts, idx, kvalid, o_t,
+                          None, o, None, ws, tau=wl.tau, keep_blocks=keep_blocks, parts=la.LA_PART_CHUNK)[1]
+    chunk_kv_ms = time_calls([chunk_kv], max(3, min(K, 10)))
+    dense_ms = None
+    if not args.no_dense and not args.profile_only:
+        dmask = torch.ones_like(mask)
+        dcounts, didx = la.mask_to_list(dmask, blk, shape.Lq, shape.Lk, d)
+        dsteps = la.bind_3d(grid, g["q"], g["k"], g["v"], q_t, k_t, v_t, qbar, kbar, dmask, dcounts, didx, kvalid,
+                            o_t, None, o, None, ws, tau=1.0)[3:6]
+        dense_ms = time_calls(dsteps, max(3, min(K, 10)))
+        del dmask, dcounts, didx, dsteps
+
+    att_ms = t["attn_plan"] + t["attn_run"] + t["attn_merge"]
+    run_ms = t["attn_run"]
+    value = kept_flops / (ms_step * 1e-3) / 1e12
+    achieved = kept_flops / (run_ms * 1e-3) / 1e12
+    bq, bkv, bkc = prep_bytes_3d(wl, "q"), prep_bytes_3d(wl, "kv"), prep_bytes_3d(wl, "kv_chunk")
+    digest = src_digest("attn.hip")
+    out = {
+        "metric": "sparse AR attention kept-block TFLOP/s (3-D blocks: prep + select + sparse attention + untile "
+                  "per call)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "H": H, "d": d, "n_text": wl.n_text, "T_ctx": wl.T_ctx,
+                   "T_q": wl.T_q, "latent": [wl.Hs, wl.Ws], "block3d": [wl.bt, wl.bh, wl.bw], "block": blk,
+                   "tau": wl.tau, "topk_r": wl.topk_r, "keep_blocks": keep_blocks, "seed": wl.seed},
+        **{f"{n}_ms": round(t[n], 4) for n in names},
+        "prep_kv_chunk_ms": round(chunk_kv_ms, 4),
+        "prep_q_gbs": round(bq / (t["prep_q"] * 1e-3) / 1e9, 1),
+        "prep_kv_gbs": round(bkv / (t["prep_kv"] * 1e-3) / 1e9, 1),
+        "prep_kv_chunk_gbs": round(bkc / (chunk_kv_ms * 1e-3) / 1e9, 1),
+        "untile_gbs": round(B * H * wl.Lq * d * 4 / (t["untile"] * 1e-3) / 1e9, 1),
+        "attn_ms": round(att_ms, 4),
+        "keep_ratio": round(rho, 5),
+        "padded_slot_fraction_q": round(1 - float(qv.sum()) / (NQ * blk), 4),
+        "kept_tflop": round(kept_flops / 1e12, 5),
+        "attn_run_tflops": round(achieved, 2),
+        "attn_run_pct_mfma_peak": round(100 * achieved / MFMA_BF16_PEAK_TFLOPS, 2),
+        "dense_attn_ms": None if dense_ms is None else round(dense_ms, 4),
+        "speedup_vs_dense": None if dense_ms is None else round(dense_ms / (t["select"] + att_ms), 3),
+        "ideal_speedup": round(1.0 / rho, 3),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": traffic_from_profile("attn_fwd", wl.name, digest, kept_flops),
+                     "kernel": f"attn_fwd_kernel<{d}>", "src_digest": digest},
+        "gpu": torch.cuda.get_device_name(dev),
+        "gen_s": round(t_gen, 2),
+    }
+    if not args.no_cpu_baseline and not args.profile_only:
+        out["cpu_baseline"] = cpu_baseline_3d(wl, inp, mask_np, qv, kv, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -144,8 +345,10 @@ def main():
         sys.exit(2)
     import torch
     from paper_2605_31158_amd import la
-    from paper_2605_31158_amd.workloads import WORKLOADS, make_inputs
+    from paper_2605_31158_amd.workloads import WORKLOADS, WORKLOADS_3D, make_inputs
 
+    if args.workload in WORKLOADS_3D:
+        return main_3d(args, WORKLOADS_3D[args.workload])
     wl = WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)

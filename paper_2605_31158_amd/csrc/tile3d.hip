@@ -79,7 +79,17 @@ __device__ inline void acc_bf16x8(float* a, u32x4 w) {
   }
 }
 
-// Lane layout: chunk c = tid % CH (16 bytes of a row), slot tid / CH + RPP p for pass p.
+// Token of every slot of block n (padding slots: the block's first token, a valid address whose
+// load is then dropped), one slot per thread, into LDS.
+template <int BLOCK>
+__device__ inline void slot_tokens(const Grid3& g, const BlockMap& bm, int* tok) {
+  for (int s = threadIdx.x; s < BLOCK; s += kTileThreads) tok[s] = bm.token(s < bm.valid ? s : 0, g);
+  __syncthreads();
+}
+
+// Lane layout: chunk c = tid % CH (16 bytes of a row), slot tid / CH + RPP p for pass p.  The
+// loads are unconditional (padding slots read the block's first token and are zeroed), so all
+// NP (K: and NP V) loads of a lane are in flight before the first store.
 template <int D, int BLOCK, int NSRC>
 __global__ __launch_bounds__(kTileThreads) void prep_kernel(const uint16_t* __restrict__ src0,
                                                             const uint16_t* __restrict__ src1,
@@ -89,31 +99,37 @@ __global__ __launch_bounds__(kTileThreads) void prep_kernel(const uint16_t* __re
   constexpr int RPP = kTileThreads / CH;
   constexpr int NP = BLOCK / RPP;
   __shared__ float red[kTileThreads / 64][D];
+  __shared__ int tok[BLOCK];
   const int n = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, c = tid % CH, r0 = tid / CH;
   const BlockMap bm = block_map<BLOCK>(g, run, n);
-  const size_t lin_base = (size_t)bh * g.Lin * D + c * 8;
-  const size_t tile_base = ((size_t)bh * g.Ltile + (size_t)(run.blk0 + n) * BLOCK) * D + c * 8;
+  slot_tokens<BLOCK>(g, bm, tok);
+  const uint16_t* s0 = src0 + (size_t)bh * g.Lin * D + c * 8;
+  const uint16_t* s1 = NSRC == 2 ? src1 + (size_t)bh * g.Lin * D + c * 8 : nullptr;
   u32x4 a[NP], b[NSRC == 2 ? NP : 1];
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
-    const int s = r0 + RPP * p;
-    a[p] = u32x4{0u, 0u, 0u, 0u};
-    if constexpr (NSRC == 2) b[p] = u32x4{0u, 0u, 0u, 0u};
-    if (s < bm.valid) {
-      const size_t off = lin_base + (size_t)bm.token(s, g) * D;
-      a[p] = *(const u32x4*)(src0 + off);
-      if constexpr (NSRC == 2) b[p] = *(const u32x4*)(src1 + off);
-    }
+    const int off = tok[r0 + RPP * p] * D;
+    a[p] = *(const u32x4*)(s0 + off);
+    if constexpr (NSRC == 2) b[p] = *(const u32x4*)(s1 + off);
   }
+  const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const bool ok = r0 + RPP * p < bm.valid;
+    a[p] = ok ? a[p] : zero;
+    if constexpr (NSRC == 2) b[p] = ok ? b[p] : zero;
+  }
+  uint16_t* d0 = dst0 + ((size_t)bh * g.Ltile + (size_t)(run.blk0 + n) * BLOCK) * D + c * 8;
+  uint16_t* d1 = NSRC == 2 ? dst1 + ((size_t)bh * g.Ltile + (size_t)(run.blk0 + n) * BLOCK) * D + c * 8 : nullptr;
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
-    const size_t off = tile_base + (size_t)(r0 + RPP * p) * D;
-    *(u32x4*)(dst0 + off) = a[p];
-    if constexpr (NSRC == 2) *(u32x4*)(dst1 + off) = b[p];
+    const int off = (r0 + RPP * p) * D;
+    *(u32x4*)(d0 + off) = a[p];
+    if constexpr (NSRC == 2) *(u32x4*)(d1 + off) = b[p];
     acc_bf16x8(acc, a[p]);
   }
   if (!bar) return;
@@ -136,6 +152,8 @@ __global__ __launch_bounds__(kTileThreads) void prep_kernel(const uint16_t* __re
   }
 }
 
+// Rows of padding slots are neither read nor written: their loads read the block's first row
+// (a valid address) and their stores are skipped.
 template <int D, int BLOCK>
 __global__ __launch_bounds__(kTileThreads) void untile_kernel(const uint16_t* __restrict__ ot,
                                                               const float* __restrict__ lset,
@@ -144,25 +162,27 @@ __global__ __launch_bounds__(kTileThreads) void untile_kernel(const uint16_t* __
   constexpr int CH = D / 8;
   constexpr int RPP = kTileThreads / CH;
   constexpr int NP = BLOCK / RPP;
+  __shared__ int tok[BLOCK];
   const int n = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, c = tid % CH, r0 = tid / CH;
   const BlockMap bm = block_map<BLOCK>(g, run, n);
+  slot_tokens<BLOCK>(g, bm, tok);
   const size_t tile_row = (size_t)bh * g.Ltile + (size_t)(run.blk0 + n) * BLOCK;
+  const uint16_t* src = ot + tile_row * D + c * 8;
+  uint16_t* dst = o + (size_t)bh * g.Lin * D + c * 8;
   u32x4 a[NP];
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     const int s = r0 + RPP * p;
-    a[p] = u32x4{0u, 0u, 0u, 0u};
-    if (s < bm.valid) a[p] = *(const u32x4*)(ot + (tile_row + s) * D + c * 8);
+    a[p] = *(const u32x4*)(src + (s < bm.valid ? s : 0) * D);
   }
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     const int s = r0 + RPP * p;
-    if (s < bm.valid) *(u32x4*)(o + ((size_t)bh * g.Lin + bm.token(s, g)) * D + c * 8) = a[p];
+    if (s < bm.valid) *(u32x4*)(dst + tok[s] * D) = a[p];
   }
   if (lse && lset) {
-    for (int s = tid; s < bm.valid; s += kTileThreads)
-      lse[(size_t)bh * g.Lin + bm.token(s, g)] = lset[tile_row + s];
+    for (int s = tid; s < bm.valid; s += kTileThreads) lse[(size_t)bh * g.Lin + tok[s]] = lset[tile_row + s];
   }
 }
 

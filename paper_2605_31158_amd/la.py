@@ -379,6 +379,38 @@ def untile_o_3d(g: Grid3D, o_tiled: torch.Tensor, lse_tiled: Optional[torch.Tens
     return o, lse
 
 
+def bind_3d(g: Grid3D, q, k, v, q_t, k_t, v_t, qbar, kbar, mask, counts, idx, kvalid, o_t, lse_t, o, lse, ws,
+            tau: Optional[float] = None, keep_blocks: Optional[int] = None, parts: int = LA_PART_ALL,
+            scale: Optional[float] = None):
+    """The 3-D path as BoundCalls on fixed tensors and the current stream:
+    (prep_q, prep_kv, select, plan, run, merge, untile); in this order they compute what
+    sparse_attn_3d computes."""
+    if (tau is None) == (keep_blocks is None):
+        raise ValueError("give exactly one of tau and keep_blocks")
+    shape = grid3d_shape(g)
+    st = _stream(q)
+    nb = ctypes.c_size_t(ws.numel())
+    keep = (g, shape, q, k, v, q_t, k_t, v_t, qbar, kbar, mask, counts, idx, kvalid, o_t, lse_t, o, lse, ws)
+    gp, sp = ctypes.byref(g), ctypes.byref(shape)
+    sc = ctypes.c_float(scale if scale is not None else 0.0)
+    prep_q = BoundCall("la_prep_q_3d", gp, _ptr(q), _ptr(q_t), _ptr(qbar), st, keep=keep)
+    prep_kv = BoundCall("la_prep_kv_3d", gp, _ptr(k), _ptr(v), ctypes.c_uint32(parts), _ptr(k_t), _ptr(v_t),
+                        _ptr(kbar), st, keep=keep)
+    if tau is not None:
+        select = BoundCall("la_select_pooled", sp, _ptr(qbar), _ptr(kbar), ctypes.c_float(tau), _ptr(mask),
+                           _ptr(counts), _ptr(idx), _ptr(ws), nb, st, keep=keep)
+    else:
+        select = BoundCall("la_select_pooled_topk", sp, _ptr(qbar), _ptr(kbar), ctypes.c_int32(keep_blocks),
+                           _ptr(mask), _ptr(counts), _ptr(idx), _ptr(ws), nb, st, keep=keep)
+    plan = BoundCall("la_sparse_attn_plan_valid", sp, _ptr(counts), _ptr(idx), _ptr(kvalid), _ptr(ws), nb, st,
+                     keep=keep)
+    run = BoundCall("la_sparse_attn_run", sp, _ptr(q_t), _ptr(k_t), _ptr(v_t), sc, _ptr(o_t), _ptr(lse_t), _ptr(ws),
+                    nb, st, keep=keep)
+    merge = BoundCall("la_sparse_attn_merge", sp, _ptr(o_t), _ptr(lse_t), _ptr(ws), nb, st, keep=keep)
+    untile = BoundCall("la_untile_o_3d", gp, _ptr(o_t), _ptr(lse_t), _ptr(o), _ptr(lse), st, keep=keep)
+    return prep_q, prep_kv, select, plan, run, merge, untile
+
+
 def sparse_attn_3d(g: Grid3D, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, tau: Optional[float] = None,
                    keep_blocks: Optional[int] = None, scale: Optional[float] = None, want_lse: bool = False,
                    kvalid: Optional[torch.Tensor] = None):

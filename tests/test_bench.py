@@ -58,3 +58,40 @@ def test_kept_flop_count_matches_oracle(Lq, Lk, block):
     NQ, NK = -(-Lq // block), -(-Lk // block)
     mask = (rng.random((2, 3, NQ, NK)) < 0.3).astype(np.uint8)
     assert bench.kept_flop_count(mask, Lq, Lk, block, 128) == O.kept_flops(mask, Lq, Lk, block, 128)
+
+
+def test_kept_flop_count_3d_matches_oracle_sets():
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D
+    wl = WORKLOADS_3D["tiny_3d"]
+    L = O.layout_3d(wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, wl.block)
+    rng = np.random.default_rng(3)
+    NQ, NK = len(L["qsets"]), len(L["ksets"])
+    mask = (rng.random((1, 2, NQ, NK)) < 0.4).astype(np.uint8)
+    want = 0
+    for h in range(2):
+        for i in range(NQ):
+            kept = np.nonzero(mask[0, h, i])[0]
+            want += 4 * wl.d * L["qsets"][i].size * sum(L["ksets"][m].size for m in kept)
+    qv = [s.size for s in L["qsets"]]
+    kv = [s.size for s in L["ksets"]]
+    assert bench.kept_flop_count_3d(mask, qv, kv, wl.d) == want
+
+
+def test_cpu_baseline_3d_on_tiny():
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D, make_inputs_3d
+    wl = WORKLOADS_3D["tiny_3d"]
+    inp = make_inputs_3d(wl)
+    L = O.layout_3d(wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, wl.block)
+    sel = O.select_blocks_sets(inp["q"], inp["k"], L["qsets"], L["ksets"], L["forced"], tau=wl.tau)
+    qv = [s.size for s in L["qsets"]]
+    kv = [s.size for s in L["ksets"]]
+    out = bench.cpu_baseline_3d(wl, inp, sel["mask"], qv, kv, target_s=0.2)
+    assert out["kind"] == "oracle" and out["value"] > 0 and "heads" in out["sample"]
+
+
+def test_prep_bytes_3d_counts_every_slot():
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D
+    wl = WORKLOADS_3D["480p_3d"]
+    # 16 heads; 52 query blocks; 3 text + 312 context + 52 chunk key blocks of 128 slots, d = 128
+    assert bench.prep_bytes_3d(wl, "q") == 16 * (6240 * 256 + 52 * 128 * 256 + 52 * 512)
+    assert bench.prep_bytes_3d(wl, "kv") == 16 * (2 * 43980 * 256 + 2 * 367 * 128 * 256 + 367 * 512)
