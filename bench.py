@@ -139,6 +139,17 @@ def cpu_baseline(wl, inp, mask_np, target_s: float):
                       f"affinity={len(os.sched_getaffinity(0))}"}
 
 
+def calibration_copy(dev):
+    """Three plain 256 MiB device copies: the known byte count the PMC byte counters are scaled by."""
+    import torch
+    src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def kept_flop_count_3d(mask_np, qvalid, kvalid, d: int) -> int:
     """kept_flop_count for blocks with padding: 4 d x (valid query tokens of the block) x (valid
     keys of the kept key blocks), summed over the kept (query block, key block) pairs."""
@@ -238,6 +249,8 @@ def main_3d(args, wl):
     stages = la.bind_3d(grid, g["q"], g["k"], g["v"], q_t, k_t, v_t, qbar, kbar, mask, counts, idx, kvalid, o_t,
                         None, o, None, ws, tau=wl.tau, keep_blocks=keep_blocks)
     names = ("prep_q", "prep_kv", "select", "attn_plan", "attn_run", "attn_merge", "untile")
+    if args.calibrate_copy:
+        calibration_copy(dev)
     for _ in range(args.warmup):
         for f in stages:
             f()
@@ -373,12 +386,7 @@ def main():
     stages = (select, plan, run, merge)
 
     if args.calibrate_copy:
-        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibration_copy(dev)
     for _ in range(args.warmup):
         for f in stages:
             f()
