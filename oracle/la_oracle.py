@@ -7,8 +7,8 @@ definition written out, one (batch, head, query block) at a time.
 
 Steps, in the paper's order and notation:
   * blocks: query blocks Q_i and key blocks K_m of `block` consecutive tokens
-    (1-D blocks; the paper tiles 3-D (B_t, B_h, B_w) blocks, Sec. 3.3 and the
-    appendix's implementation details);
+    (1-D blocks, as the benchmark configurations use; the 3-D blocks of the paper
+    are the second section below);
   * pooled proxies q_bar_i and k_bar_m: means over each block's tokens
     (Sec. 3.3, pooling equation);
   * relevance s_{i,m} = q_bar_i . k_bar_m / sqrt(d) over the M historical blocks
@@ -31,8 +31,14 @@ Readings where the paper is silent (each is listed in the design notes too):
     <= f; the whole context stays visible (subject to block selection);
   * a query token with no visible key gets o = 0 and lse = -inf.
 
-Parity pins live in tests/test_oracle.py (closed forms, brute force, library
-attention, invariants); nothing here is checked against itself.
+A second section builds the same steps over 3-D (B_t, B_h, B_w) blocks given as token sets
+(Sec. 3.3 and the appendix's block sizes), and a third holds the scalar policy around the
+path: latent dynamics, its moving average and the temporal window (Sec. 3.1), the
+pose-similarity gate (Sec. 3.1) and the denoising-cache schedule (Sec. 3.2).
+
+Parity pins live in tests/test_oracle.py, tests/test_oracle_3d.py and
+tests/test_oracle_policy.py (closed forms, brute force, library attention, invariants);
+nothing here is checked against itself.
 """
 from __future__ import annotations
 
@@ -463,3 +469,67 @@ def attention_sets_rows(q, k, v, qsets, ksets, mask, rows: Iterable[Tuple[int, i
         ok = np.ones((qi.size, cand.size), dtype=bool)
         out[(b, h, i)] = attention_block(qh[qi], kh[cand], vh[cand], ok, scale)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Adaptive context management (Sec. 3.1) and the denoising cache (Sec. 3.2): the scalar policy
+# around the attention path.  Camera-pose similarities are inputs (the paper instantiates them
+# with an FOV overlap it does not define).
+
+def latent_mse(z_prev: np.ndarray, z_prev2: np.ndarray) -> float:
+    """D_t = MSE(z_{t-1}, z_{t-2}), the mean over every latent dimension of the squared
+    difference of the two most recent stable units (Sec. 3.1, latent-dynamics equation).
+    Arrays of one size (uint16 = bf16 bit patterns); the sum is exact (math.fsum)."""
+    a = _as_f64(z_prev).ravel()
+    b = _as_f64(z_prev2).ravel()
+    if a.size != b.size or a.size == 0:
+        raise ValueError("two non-empty latents of one size are needed")
+    return math.fsum(((a - b) ** 2).tolist()) / a.size
+
+
+def ema_dynamics(D_t: float, D_bar_prev: Optional[float], alpha: float) -> float:
+    """D_bar_t = alpha D_t + (1 - alpha) D_bar_{t-1}, started by the first valid D_t
+    (D_bar_prev None) (Sec. 3.1, smoothing equation); alpha in (0, 1]."""
+    if not (0.0 < alpha <= 1.0):
+        raise ValueError("alpha must lie in (0, 1]")
+    if D_bar_prev is None:
+        return float(D_t)
+    return alpha * D_t + (1.0 - alpha) * D_bar_prev
+
+
+def temporal_window(D_bar: float, kappa: float, L_m: int) -> int:
+    """L_t = clip(floor(L_m kappa / (D_bar + kappa)), 1, L_m) (Sec. 3.1, window equation);
+    kappa > 0, L_m >= 1, D_bar >= 0."""
+    if not (kappa > 0.0) or L_m < 1 or not (D_bar >= 0.0):
+        raise ValueError("kappa > 0, L_m >= 1 and D_bar >= 0 are needed")
+    return int(min(max(math.floor(L_m * kappa / (D_bar + kappa)), 1), L_m))
+
+
+def revisiting(similarities: Sequence[float], tau_pose: float) -> bool:
+    """max_j S_pose(t, j) >= tau_pose: a reliable pose-aware reference exists (Sec. 3.1 gate
+    and Sec. 3.2 reuse condition).  False (pure exploration) also when there is no candidate."""
+    return len(similarities) > 0 and max(float(s) for s in similarities) >= tau_pose
+
+
+def keep_retrieved_memory(similarities: Sequence[float], tau_pose: float) -> bool:
+    """Retrieved spatial memory is kept unless the step is pure exploration, i.e. the largest
+    similarity is below tau_pose (Sec. 3.1, retrieved-memory gate)."""
+    return revisiting(similarities, tau_pose)
+
+
+def model_calls(K: int, reuse: bool) -> List[bool]:
+    """Which of the K denoising steps evaluate the model (Sec. 3.2): with reuse (revisiting)
+    and K > 2, only the first and the last; steps 1..K-2 reuse the first output.  Otherwise
+    every step."""
+    if K < 1:
+        raise ValueError("K >= 1")
+    if not reuse or K <= 2:
+        return [True] * K
+    return [i == 0 or i == K - 1 for i in range(K)]
+
+
+def reuse_source(K: int, reuse: bool) -> List[int]:
+    """For each of the K steps, the step whose model output it uses: itself, or step 0 for
+    the reused intermediate steps (Sec. 3.2, reuse equation)."""
+    calls = model_calls(K, reuse)
+    return [i if calls[i] else 0 for i in range(K)]
