@@ -345,6 +345,18 @@ def main_3d(args, wl):
         "gpu": torch.cuda.get_device_name(dev),
         "gen_s": round(t_gen, 2),
     }
+    # latent dynamics (Sec. 3.1) once per AR step: a chunk latent of 4 frames of 30x52 tokens x 64
+    # values (fp32), and a 256 Mi-value pair that shows the kernel's bandwidth
+    mse = {}
+    for label, nval in (("chunk", wl.T_q * wl.Hs * wl.Ws * 64), ("256Mi", 1 << 28)):
+        za = torch.randn(nval, device=dev)
+        zb = torch.randn(nval, device=dev)
+        mws = torch.empty(la.LATENT_MSE_WS_BYTES, dtype=torch.uint8, device=dev)
+        mout = torch.empty(1, dtype=torch.float64, device=dev)
+        ms = time_calls([lambda: la.latent_mse(za, zb, ws=mws, out=mout)], 20)
+        mse[label] = {"values": nval, "us": round(ms * 1e3, 2), "gbs": round(2 * 4 * nval / (ms * 1e-3) / 1e9, 1)}
+        del za, zb
+    out["latent_mse"] = mse
     if not args.no_cpu_baseline and not args.profile_only:
         out["cpu_baseline"] = cpu_baseline_3d(wl, inp, mask_np, qv, kv, args.cpu_seconds)
     print(json.dumps(out), flush=True)

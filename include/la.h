@@ -243,6 +243,50 @@ la_status la_sparse_attn_plan_valid(const la_shape* shape, const int32_t* counts
 la_status la_untile_o_3d(const la_grid3d* grid, const void* o_tiled, const float* lse_tiled, void* o,
                          float* lse, void* stream);
 
+/* ------------------------------------------------------------------------------
+ * The scalar policy around the path: adaptive context management (Sec. 3.1) and the
+ * denoising cache (Sec. 3.2).  Only the latent dynamics runs on the GPU; the other
+ * calls are host-only scalar rules (no GPU, no stream), exact in double precision.
+ * Camera-pose similarities are inputs: the paper instantiates them with an FOV
+ * overlap measure it does not define.
+ * -------------------------------------------------------------------------- */
+typedef enum la_dtype { LA_DTYPE_F32 = 0, LA_DTYPE_BF16 = 1 } la_dtype;
+
+/* Workspace bytes of la_latent_mse (fp64 partial sums; 256-byte aligned). */
+#define LA_LATENT_MSE_WS_BYTES 8192
+
+/* Latent dynamics D_t = MSE(z_{t-1}, z_{t-2}) (Sec. 3.1, latent-dynamics equation): the mean
+ * over all n values of (z_a - z_b)^2.
+ *   z_a, z_b  device arrays of n values of `dtype` (fp32 or bf16), 16-byte aligned; any
+ *             layout, the same for both (the mean runs over every latent dimension).
+ *   out       device double: D_t.  Squares are summed in fp32 within 16-byte chunks and in
+ *             fp64 beyond; the order is fixed by n, so the result is bit-reproducible.
+ *   ws        LA_LATENT_MSE_WS_BYTES of device scratch.
+ * n < 1, a bad dtype, NULL or misaligned pointers are LA_ERR_ARG. */
+la_status la_latent_mse(const void* z_a, const void* z_b, int64_t n, int32_t dtype, double* out,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Host-only.  Moving average D_bar_t = alpha D_t + (1 - alpha) D_bar_{t-1} (Sec. 3.1,
+ * smoothing equation); D_bar_prev NULL starts the average with D_t.  alpha in (0, 1],
+ * D_t >= 0, else LA_ERR_ARG. */
+la_status la_dynamics_ema(double D_t, const double* D_bar_prev, double alpha, double* D_bar);
+
+/* Host-only.  Temporal window L_t = clip(floor(L_m kappa / (D_bar + kappa)), 1, L_m)
+ * (Sec. 3.1, window equation).  kappa > 0, L_m >= 1, D_bar >= 0, else LA_ERR_ARG. */
+la_status la_temporal_window(double D_bar, double kappa, int32_t L_m, int32_t* L_t);
+
+/* Host-only.  Pose gate (Sec. 3.1 retrieved-memory gate, Sec. 3.2 reuse condition):
+ * *revisiting = 1 when max_j similarities[j] >= tau_pose (keep the retrieved memory, allow
+ * denoising reuse), 0 for pure exploration or n = 0 (discard the retrieved memory).
+ * similarities: host array of n floats; NaN entries are LA_ERR_ARG. */
+la_status la_pose_revisiting(const float* similarities, int32_t n, float tau_pose, int32_t* revisiting);
+
+/* Host-only.  Denoising-cache schedule over K steps (Sec. 3.2, reuse equation): source[i] =
+ * the step whose model output step i uses, i for an evaluated step and 0 for the reused
+ * intermediate steps 1..K-2 when reuse != 0 and K > 2; the model is evaluated at steps i with
+ * source[i] == i.  source: host array of K int32.  K < 1 is LA_ERR_ARG. */
+la_status la_denoise_schedule(int32_t K, int32_t reuse, int32_t* source);
+
 /* Static description of a status code. */
 const char* la_status_string(la_status status);
 

@@ -259,6 +259,47 @@ la_status la_untile_o_3d(const la_grid3d* grid, const void* o_tiled, const float
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 
+la_status la_latent_mse(const void* z_a, const void* z_b, int64_t n, int32_t dtype, double* out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  if (!z_a || !z_b || !out || n < 1) return LA_ERR_ARG;
+  if (dtype != LA_DTYPE_F32 && dtype != LA_DTYPE_BF16) return LA_ERR_ARG;
+  if (misaligned(z_a) || misaligned(z_b) || ((uintptr_t)out & 7u)) return LA_ERR_ARG;
+  if (!ws || ws_bytes < LA_LATENT_MSE_WS_BYTES || ((uintptr_t)ws & 255u)) return LA_ERR_WORKSPACE;
+  hipError_t e = launch_latent_mse(z_a, z_b, n, dtype == LA_DTYPE_BF16, out, ws, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
+la_status la_dynamics_ema(double D_t, const double* D_bar_prev, double alpha, double* D_bar) {
+  if (!D_bar || !(alpha > 0.0 && alpha <= 1.0) || !(D_t >= 0.0)) return LA_ERR_ARG;
+  if (D_bar_prev && !(*D_bar_prev >= 0.0)) return LA_ERR_ARG;
+  *D_bar = D_bar_prev ? alpha * D_t + (1.0 - alpha) * *D_bar_prev : D_t;
+  return LA_OK;
+}
+
+la_status la_temporal_window(double D_bar, double kappa, int32_t L_m, int32_t* L_t) {
+  if (!L_t || !(kappa > 0.0) || L_m < 1 || !(D_bar >= 0.0)) return LA_ERR_ARG;
+  const double x = floor((double)L_m * kappa / (D_bar + kappa));
+  *L_t = x < 1.0 ? 1 : (x > (double)L_m ? L_m : (int32_t)x);
+  return LA_OK;
+}
+
+la_status la_pose_revisiting(const float* similarities, int32_t n, float tau_pose, int32_t* revisiting) {
+  if (!revisiting || n < 0 || (n > 0 && !similarities) || isnan(tau_pose)) return LA_ERR_ARG;
+  float mx = -INFINITY;
+  for (int32_t j = 0; j < n; ++j) {
+    if (isnan(similarities[j])) return LA_ERR_ARG;
+    mx = similarities[j] > mx ? similarities[j] : mx;
+  }
+  *revisiting = (n > 0 && mx >= tau_pose) ? 1 : 0;
+  return LA_OK;
+}
+
+la_status la_denoise_schedule(int32_t K, int32_t reuse, int32_t* source) {
+  if (K < 1 || !source) return LA_ERR_ARG;
+  for (int32_t i = 0; i < K; ++i) source[i] = (reuse && K > 2 && i > 0 && i < K - 1) ? 0 : i;
+  return LA_OK;
+}
+
 const char* la_status_string(la_status s) {
   switch (s) {
     case LA_OK: return "ok";

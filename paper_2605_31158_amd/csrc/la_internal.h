@@ -70,6 +70,13 @@ hipError_t launch_prep_kv(const G3Dims& gd, const void* k, const void* v, uint32
 hipError_t launch_untile_o(const G3Dims& gd, const void* o_tiled, const float* lse_tiled, void* o, float* lse,
                            hipStream_t st);
 
+// Latent dynamics (Sec. 3.1): mean squared difference of two latents of n values (fp32 or bf16)
+// into out[0] (fp64), through at most kMseMaxBlocks fp64 partials in ws.
+constexpr int kMseMaxBlocks = 1024;
+int mse_blocks(int64_t n, int bf16);
+hipError_t launch_latent_mse(const void* a, const void* b, int64_t n, int bf16, double* out, void* ws,
+                             hipStream_t st);
+
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace la

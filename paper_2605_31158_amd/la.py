@@ -69,6 +69,11 @@ _SIGNATURES = {
                                                 ctypes.c_size_t, _P]),
     "la_sparse_attn_plan_valid": (ctypes.c_int, [_SP, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_untile_o_3d": (ctypes.c_int, [_GP, _P, _P, _P, _P, _P]),
+    "la_latent_mse": (ctypes.c_int, [_P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, ctypes.c_size_t, _P]),
+    "la_dynamics_ema": (ctypes.c_int, [ctypes.c_double, _P, ctypes.c_double, _P]),
+    "la_temporal_window": (ctypes.c_int, [ctypes.c_double, ctypes.c_double, ctypes.c_int32, _P]),
+    "la_pose_revisiting": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_float, _P]),
+    "la_denoise_schedule": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, _P]),
     "la_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "la_abi_version": (ctypes.c_int32, []),
 }
@@ -429,6 +434,68 @@ def sparse_attn_3d(g: Grid3D, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
     o_t, lse_t = res if want_lse else (res, None)
     o, lse = untile_o_3d(g, o_t, lse_t)
     return o, lse, mask, counts, idx
+
+
+# ----------------------------------------------------------------------------------------------
+# scalar policy (Sec. 3.1, Sec. 3.2)
+
+LA_DTYPE_F32, LA_DTYPE_BF16 = 0, 1
+LATENT_MSE_WS_BYTES = 8192
+
+
+def latent_mse(z_a: torch.Tensor, z_b: torch.Tensor, ws: Optional[torch.Tensor] = None,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """D_t = MSE(z_a, z_b) over every value (fp32 or bf16 GPU tensors of one shape) -> float64
+    GPU tensor of one element."""
+    for name, t in (("z_a", z_a), ("z_b", z_b)):
+        if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous GPU tensor")
+    if z_a.dtype != z_b.dtype or z_a.shape != z_b.shape:
+        raise ValueError("z_a and z_b must have one dtype and one shape")
+    dt = {torch.float32: LA_DTYPE_F32, torch.bfloat16: LA_DTYPE_BF16}.get(z_a.dtype)
+    if dt is None:
+        raise TypeError("latents must be float32 or bfloat16")
+    if ws is None:
+        ws = torch.empty(LATENT_MSE_WS_BYTES, dtype=torch.uint8, device=z_a.device)
+    if out is None:
+        out = torch.empty(1, dtype=torch.float64, device=z_a.device)
+    _call("la_latent_mse", _ptr(z_a), _ptr(z_b), ctypes.c_int64(z_a.numel()), ctypes.c_int32(dt), _ptr(out),
+          _ptr(ws), ctypes.c_size_t(ws.numel()), _stream(z_a))
+    return out
+
+
+def dynamics_ema(D_t: float, D_bar_prev: Optional[float], alpha: float) -> float:
+    """D_bar_t = alpha D_t + (1 - alpha) D_bar_{t-1}; None starts the average (host only)."""
+    res = ctypes.c_double()
+    prev = None if D_bar_prev is None else ctypes.byref(ctypes.c_double(D_bar_prev))
+    _call("la_dynamics_ema", ctypes.c_double(D_t), prev, ctypes.c_double(alpha), ctypes.byref(res))
+    return res.value
+
+
+def temporal_window(D_bar: float, kappa: float, L_m: int) -> int:
+    """L_t = clip(floor(L_m kappa / (D_bar + kappa)), 1, L_m) (host only)."""
+    res = ctypes.c_int32()
+    _call("la_temporal_window", ctypes.c_double(D_bar), ctypes.c_double(kappa), ctypes.c_int32(L_m),
+          ctypes.byref(res))
+    return res.value
+
+
+def pose_revisiting(similarities, tau_pose: float) -> bool:
+    """max_j similarities[j] >= tau_pose (host only; float32 comparisons)."""
+    import numpy as np
+    sims = np.ascontiguousarray(similarities, dtype=np.float32)
+    res = ctypes.c_int32()
+    _call("la_pose_revisiting", sims.ctypes.data_as(_P) if sims.size else None, ctypes.c_int32(sims.size),
+          ctypes.c_float(tau_pose), ctypes.byref(res))
+    return bool(res.value)
+
+
+def denoise_schedule(K: int, reuse: bool):
+    """For each of the K denoising steps, the step whose model output it uses (host only)."""
+    import numpy as np
+    src = np.zeros(max(K, 1), dtype=np.int32)
+    _call("la_denoise_schedule", ctypes.c_int32(K), ctypes.c_int32(1 if reuse else 0), src.ctypes.data_as(_P))
+    return [int(x) for x in src[:K]]
 
 
 def bf16_from_bits(bits, device="cuda") -> torch.Tensor:
