@@ -139,6 +139,14 @@ def cpu_baseline(wl, inp, mask_np, target_s: float):
                       f"affinity={len(os.sched_getaffinity(0))}"}
 
 
+def device_info(dev) -> dict:
+    """Name, architecture, compute units and memory of the device, and the HIP version torch uses."""
+    import torch
+    p = torch.cuda.get_device_properties(dev)
+    return {"name": p.name, "arch": getattr(p, "gcnArchName", None), "cus": p.multi_processor_count,
+            "mem_gib": round(p.total_memory / 2**30, 1), "hip": torch.version.hip}
+
+
 def calibration_copy(dev):
     """Three plain 256 MiB device copies: the known byte count the PMC byte counters are scaled by."""
     import torch
@@ -342,7 +350,7 @@ def main_3d(args, wl):
                      "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
                      "traffic": traffic_from_profile("attn_fwd", wl.name, digest, kept_flops),
                      "kernel": f"attn_fwd_kernel<{d}>", "src_digest": digest},
-        "gpu": torch.cuda.get_device_name(dev),
+        "gpu": device_info(dev),
         "gen_s": round(t_gen, 2),
     }
     # latent dynamics (Sec. 3.1) once per AR step: a chunk latent of 4 frames of 30x52 tokens x 64
@@ -489,7 +497,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
                      "traffic": traffic, "kernel": f"attn_fwd_kernel<{d}>", "src_digest": digest},
-        "gpu": torch.cuda.get_device_name(dev),
+        "gpu": device_info(dev),
         "gen_s": round(t_gen, 2),
     }
     if not args.no_cpu_baseline and not args.profile_only:
