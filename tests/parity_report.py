@@ -5,7 +5,9 @@
 For every workload: the GPU block mask against the fp64 oracle's (entries that differ, and
 entries that differ outside the ambiguity band), then the GPU attention output on the GPU's
 own mask against the oracle on sampled query blocks (every block for the tiny workload):
-max-abs and mean-abs error of o and max-abs error of lse.  The same checks, with the same
+max-abs and mean-abs error of o and max-abs error of lse.  The 3-D workloads run the whole
+3-D path (prep, selection from pooled means, attention, untile) against the oracle's
+block-set definitions.  The same checks, with the same
 bars, are asserted by the GPU tests; this script prints the numbers."""
 import os
 import sys
@@ -69,12 +71,67 @@ def report(name, samples=24):
     return int(outside.sum()) == 0 and mx <= 2e-2 and mean_sum / max(n, 1) <= 2e-3
 
 
+def report_3d(name, samples=12):
+    """The 3-D layout path: GPU mask over the tiled blocks against the oracle's block-set
+    selection, and the linear-order output against the oracle's attention on sampled blocks."""
+    import torch
+    from paper_2605_31158_amd import la
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D, make_inputs_3d
+    wl = WORKLOADS_3D[name]
+    inp = make_inputs_3d(wl)
+    g = {x: la.bf16_from_bits(inp[x]) for x in "qkv"}
+    grid = la.grid3d(wl.B, wl.H, wl.d, wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, wl.block)
+    L = O.layout_3d(wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, wl.block)
+    M = int((~L["forced"]).sum())
+    if wl.tau is not None:
+        gargs, oargs = dict(tau=wl.tau), dict(tau=wl.tau)
+    else:
+        gargs, oargs = dict(keep_blocks=int(np.floor(wl.topk_r * M))), dict(topk_r=wl.topk_r)
+    o, lse, mask, counts, idx = la.sparse_attn_3d(grid, g["q"], g["k"], g["v"], want_lse=True, **gargs)
+    torch.cuda.synchronize()
+    mask_np = mask.cpu().numpy()
+    o_np = o.float().cpu().numpy().astype(np.float64)
+    lse_np = lse.cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    sel = O.select_blocks_sets(inp["q"], inp["k"], L["qsets"], L["ksets"], L["forced"], **oargs)
+    t_sel = time.perf_counter() - t0
+    diff = mask_np != sel["mask"]
+    outside = diff & ~O.ambiguous_blocks(sel, 1e-4)
+    NQ = len(L["qsets"])
+    rng = np.random.default_rng(2024)
+    rows = sorted({(0, int(h), int(i)) for h, i in zip(rng.integers(0, wl.H, samples), rng.integers(0, NQ, samples))}
+                  | {(0, 0, NQ - 1)})
+    t0 = time.perf_counter()
+    ref = O.attention_sets_rows(inp["q"], inp["k"], inp["v"], L["qsets"], L["ksets"], mask_np, rows)
+    t_att = time.perf_counter() - t0
+    mx = mean_sum = lse_mx = 0.0
+    n = 0
+    for (b, h, i), (ob, lb) in ref.items():
+        qi = L["qsets"][i]
+        d = np.abs(o_np[b, h, qi] - ob)
+        mx = max(mx, float(d.max()))
+        mean_sum += float(d.sum())
+        n += d.size
+        lse_mx = max(lse_mx, float(np.abs(lse_np[b, h, qi] - lb).max()))
+    qv = np.array([s.size for s in L["qsets"]])
+    kv = np.array([s.size for s in L["ksets"]])
+    kept = (mask_np.astype(np.int64) * qv[:, None] * kv[None, :]).sum()
+    rho = kept / float(wl.B * wl.H * qv.sum() * kv.sum())
+    print(f"| {name} | {rho:.4f} | {int(diff.sum())} of {diff.size} | {int(outside.sum())} | {len(rows)} | "
+          f"{mx:.2e} | {mean_sum / max(n, 1):.2e} | {lse_mx:.2e} | {t_sel:.1f} / {t_att:.1f} |", flush=True)
+    return int(outside.sum()) == 0 and mx <= 2e-2 and mean_sum / max(n, 1) <= 2e-3
+
+
+DEFAULT_3D = ["tiny_3d", "480p_3d", "720p_3d"]
+
+
 def main():
-    names = sys.argv[1:] or DEFAULT
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D
+    names = sys.argv[1:] or DEFAULT + DEFAULT_3D
     print("| workload | kept ratio | mask entries differing | outside the 1e-4 band | query blocks compared | "
           "o max-abs | o mean-abs | lse max-abs | oracle s (select / attention rows) |")
     print("|---|---|---|---|---|---|---|---|---|")
-    ok = all([report(n) for n in names])
+    ok = all([report_3d(n) if n in WORKLOADS_3D else report(n) for n in names])
     sys.exit(0 if ok else 1)
 
 
