@@ -55,6 +55,8 @@ SMALL = {
     "mg_small": Workload3D("mg_small", 2, 1, 128, 0, 4, 4, 45, 80, 4, 4, 8, 128, 22, 2, 0, topk_r=0.175),
     # d = 64 with 64-slot blocks of 2x4x8 = 64 tokens, no text, single chunk frame
     "d64_b64": Workload3D("d64_b64", 1, 3, 64, 0, 6, 1, 12, 20, 2, 4, 8, 64, 23, 2, 1, tau=0.8),
+    # no context frames (M = 0): text (exactly two blocks) and chunk only
+    "no_ctx": Workload3D("no_ctx", 1, 2, 64, 128, 0, 3, 7, 10, 2, 3, 4, 64, 24, 0, 0, tau=0.9),
 }
 
 
@@ -242,3 +244,35 @@ def test_named_3d_workloads(name):
     pick = sorted({0, NQ - 1, *rng.integers(0, NQ, size=4).tolist()})
     rows = [(0, int(h), i) for i, h in zip(pick, rng.integers(0, wl.H, size=len(pick)))]
     compare_rows(o, lse, inp, L, mask, rows, name)
+
+
+@pytest.mark.parametrize("block", [64, 128])
+def test_kvalid_truncates_key_blocks(block):
+    # any valid counts per key block (0, partial, full): attention sees the first kvalid[m] keys
+    # of every kept block m, as the oracle over the truncated block sets
+    rng = np.random.default_rng(block)
+    B, H, d, NQ, NK = 1, 2, 128, 3, 9
+    Lq, Lk = NQ * block, NK * block
+    from paper_2605_31158_amd.workloads import make_clustered
+    inp = make_clustered(B, H, Lq, Lk, d, block, 40 + block)
+    kv = rng.integers(0, block + 1, size=NK).astype(np.int32)
+    kv[0], kv[-1] = 0, block // 2 + 3
+    mask = (rng.uniform(size=(B, H, NQ, NK)) < 0.6).astype(np.uint8)
+    mask[..., -1] = 1
+    g = to_gpu(inp)
+    counts, idx = la.mask_to_list(torch.from_numpy(mask).cuda(), block, Lq, Lk, d)
+    o, lse = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, block, want_lse=True,
+                                kvalid=torch.from_numpy(kv).cuda())
+    torch.cuda.synchronize()
+    qsets = [np.arange(i * block, (i + 1) * block) for i in range(NQ)]
+    ksets = [np.arange(m * block, m * block + kv[m]) for m in range(NK)]
+    rows = [(0, h, i) for h in range(H) for i in range(NQ)]
+    ref = O.attention_sets_rows(inp["q"], inp["k"], inp["v"], qsets, ksets, mask, rows)
+    o_np, lse_np = bf16_tensor_to_f64(o), lse.cpu().numpy().astype(np.float64)
+    for (b, h, i), (ob, lb) in ref.items():
+        rs = slice(i * block, (i + 1) * block)
+        assert_attn_close(o_np[b, h, rs], ob, f"kvalid block {block} row {(b, h, i)}")
+        fin = np.isfinite(lb)
+        assert np.isneginf(lse_np[b, h, rs][~fin]).all()
+        if fin.any():
+            assert np.abs(lse_np[b, h, rs][fin] - lb[fin]).max() <= LSE_TOL
