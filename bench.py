@@ -490,6 +490,9 @@ def main():
         "attn_run_tflops": round(achieved, 2),
         "attn_run_pct_mfma_peak": round(100 * achieved / MFMA_BF16_PEAK_TFLOPS, 2),
         "select_gbs": round(hbm_sel_bytes / (sel_ms * 1e-3) / 1e9, 1),
+        "select_pct_hbm_peak": round(100 * hbm_sel_bytes / (sel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 1),
+        "median_ms": {"select": round(float(np.median(t_sel)), 4), "attn": round(float(np.median(t_att)), 4),
+                      "attn_run": round(float(np.median(t_run)), 4)},
         "dense_attn_ms": None if dense_ms is None else round(dense_ms, 4),
         "dense_tflops": None if dense_ms is None else round(dense_flops / (dense_ms * 1e-3) / 1e12, 2),
         "speedup_vs_dense": None if dense_ms is None else round(dense_ms / (sel_ms + att_ms), 3),
