@@ -51,3 +51,23 @@ def test_frame_structure_shares_centroids_with_chunk():
 def test_clustered_helper():
     inp = make_clustered(2, 3, Lq=70, Lk=200, d=16, block=32, seed=1, v_kind="index")
     assert inp["q"].shape == (2, 3, 70, 16) and inp["v"].shape == (2, 3, 200, 16)
+
+
+def test_3d_generator_is_seeded_and_follows_its_recipe():
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D, make_inputs_3d
+    wl = WORKLOADS_3D["tiny_3d"]
+    a, b = make_inputs_3d(wl), make_inputs_3d(wl)
+    for x in "qkv":
+        np.testing.assert_array_equal(a[x], b[x])
+    assert a["q"].shape == (wl.B, wl.H, wl.Lq, wl.d) and a["k"].shape == (wl.B, wl.H, wl.Lk, wl.d)
+    c = make_inputs_3d(wl.replace(seed=wl.seed + 1))
+    assert not np.array_equal(a["k"], c["k"])
+    # recipe: a chunk query and the chunk key at the same position share a centroid (noise 0.5 each),
+    # tokens of different regions do not
+    f = lambda bits: (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    q, k = f(a["q"][0, 0]), f(a["k"][0, 0])
+    ck = k[wl.n_text + wl.T_ctx * wl.frame_tokens:]
+    same = np.mean(np.sum(q * ck, axis=1)) / wl.d
+    assert 0.6 < same < 1.6, same        # centroid variance ~1 (random walk), noise uncorrelated
+    other = np.mean(np.sum(q[: wl.Ws] * np.roll(ck[: wl.Ws], wl.bw, axis=0), axis=1)) / wl.d
+    assert abs(other) < 0.4, other
