@@ -335,11 +335,12 @@ __device__ __forceinline__ void softmax_tile(f32x16* sacc, bf16x8* pb, f32x16* o
 // Work plan.  The query blocks of each (batch, head) bh are ordered by the first historical key
 // block they keep and cut into groups of NL = 256 / block: unit u = (bh, g) holds query blocks
 // qmap[u NL + L], L < NL (-1 past the last block).  Its tiles are the 64-key sub-tiles of the
-// union of its lists in ascending block order; ulist[u NK + i] = block << 4 | ownership bits
-// (bit L: list L keeps the block), ucount[u] = blocks * (block / 64) sub-tiles.  The unit's
-// tiles number max(1, ucount[u]): an empty unit gets one unowned tile, so that some workgroup
-// writes its output.  The grouping only decides which rows
-// share K/V tiles: any grouping gives the same result.
+// union of its lists in ascending block order, leaving out sub-tiles without a visible key (past
+// Lk, or past the block's valid count); ulist[u NK (block / 64) + i] = block << 5 | sub-tile << 4
+// | ownership bits (bit L: list L keeps the block), ucount[u] = sub-tiles.  The unit's tiles
+// number max(1, ucount[u]): an empty unit gets one unowned tile, so that some workgroup writes
+// its output.  The grouping only decides which rows share K/V tiles: any grouping gives the same
+// result.
 
 constexpr int kPlanThreads = 256;
 constexpr int kMaxGroupNQ = 1024;   // heads with more query blocks keep the natural order
@@ -384,12 +385,22 @@ __device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
   return base + incl - x;
 }
 
+// 64-key sub-tiles of key block j that hold a visible key: the block's keys below Lk and, with
+// kvalid, its first kvalid[j] keys (clamped to [0, block]); sub-tiles with none are left out of
+// the plan (they would contribute nothing but masked MFMA work).
+__device__ inline int block_subtiles(int j, int Lk, int block, const int32_t* __restrict__ kvalid) {
+  int v = min(block, Lk - j * block);
+  if (kvalid) v = min(v, min(max(kvalid[j], 0), block));
+  return (v + KT - 1) / KT;
+}
+
 // One workgroup per unit: its query blocks (rank by (key, block index) inside the head) and the
-// union of their lists with ownership bits.
+// union of their lists with ownership bits, expanded into the sub-tiles that hold visible keys.
 __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t* __restrict__ counts,
                                                                   const int32_t* __restrict__ idx,
-                                                                  const int32_t* __restrict__ keys, int NQ, int NK,
-                                                                  int block, int row_tiles,
+                                                                  const int32_t* __restrict__ keys,
+                                                                  const int32_t* __restrict__ kvalid, int NQ, int NK,
+                                                                  int Lk, int block, int row_tiles,
                                                                   int32_t* __restrict__ qmap,
                                                                   int32_t* __restrict__ ulist,
                                                                   int32_t* __restrict__ ucount) {
@@ -442,20 +453,24 @@ __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t*
   for (int wi = w0; wi < w1; ++wi) {
     const uint32_t x = own[wi];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) cnt += ((x >> (4 * e)) & 15u) ? 1 : 0;
+    for (int e = 0; e < 8; ++e)
+      if ((x >> (4 * e)) & 15u) cnt += block_subtiles(8 * wi + e, Lk, block, kvalid);
   }
   int total;
   int pos = block_excl_scan_i(cnt, sh, &total);
-  int32_t* out = ulist + (size_t)u * NK;
+  int32_t* out = ulist + (size_t)u * NK * nsub;
   for (int wi = w0; wi < w1; ++wi) {
     const uint32_t x = own[wi];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const uint32_t bits = (x >> (4 * e)) & 15u;
-      if (bits) out[pos++] = ((8 * wi + e) << 4) | (int)bits;
+      if (!bits) continue;
+      const int j = 8 * wi + e;
+      const int ns = block_subtiles(j, Lk, block, kvalid);
+      for (int sub = 0; sub < ns; ++sub) out[pos++] = (j << 5) | (sub << 4) | (int)bits;
     }
   }
-  if (tid == 0) ucount[u] = total * nsub;
+  if (tid == 0) ucount[u] = total;
 }
 
 // Expands unit u's union list into one record per 64-key tile at its place tstart[u] in the
@@ -487,16 +502,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t*
     if (u == U - 1) tstart[U] = ts + n;
   }
   int4* out = trec + ts;
-  const int32_t* ul = ulist + (size_t)u * NK;
+  const int32_t* ul = ulist + (size_t)u * NK * nsub;
   for (int a = tid; a < n; a += kPlanThreads) {
     int key0 = 0, bits = 0;
     if (nt > 0) {
-      const int e = ul[nsub == 2 ? (a >> 1) : a];
-      const int sub = nsub == 2 ? (a & 1) : 0;
-      key0 = (e >> 4) * block + sub * KT;
+      const int e = ul[a];
+      const int j = e >> 5, sub = (e >> 4) & 1;
+      key0 = j * block + sub * KT;
       bits = e & 15;
       if (kvalid) {
-        const int kv = min(max(kvalid[e >> 4], 0), block) - sub * KT;
+        const int kv = min(max(kvalid[j], 0), block) - sub * KT;
         bits |= (KT - min(max(kv, 0), KT)) << kFlPadShift;
       }
     }
@@ -944,7 +959,7 @@ AttnWs attn_ws_layout(const Dims& dm, void* base) {
   w.keys = (int32_t*)(b + off);
   off += align256((size_t)dm.BH * dm.NQ * sizeof(int32_t));
   w.ulist = (int32_t*)(b + off);
-  off += align256(U * (size_t)dm.NK * sizeof(int32_t));
+  off += align256(U * (size_t)dm.NK * (dm.block / KT) * sizeof(int32_t));
   w.ucount = (int32_t*)(b + off);
   off += align256(U * sizeof(int32_t));
   w.tstart = (int32_t*)(b + off);
@@ -983,7 +998,8 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
   hipLaunchKernelGGL(plan_keys_kernel, dim3(ceil_div(rows, kPlanThreads / 64)), dim3(kPlanThreads), 0, st, counts,
                      idx, rows, dm.NK, dm.h0, dm.h1, w.keys);
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
-                     st, counts, idx, w.keys, dm.NQ, dm.NK, dm.block, row_tiles, w.qmap, w.ulist, w.ucount);
+                     st, counts, idx, w.keys, kvalid, dm.NQ, dm.NK, dm.Lk, dm.block, row_tiles, w.qmap, w.ulist,
+                     w.ucount);
   hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U, dm.NK,
                      dm.block, row_tiles, w.trec, w.tstart);
   return hipGetLastError();
