@@ -211,8 +211,21 @@ la_status la_prep_q_3d(const la_grid3d* grid, const void* q, void* q_tiled, floa
 la_status la_prep_kv_3d(const la_grid3d* grid, const void* k, const void* v, uint32_t parts,
                         void* k_tiled, void* v_tiled, float* kbar, void* stream);
 
+/* Block means of a 1-D block layout (Sec. 3.3, pooling equation), for callers that keep the
+ * key means of the context across calls (the context keys do not change between the
+ * denoising steps of a chunk; the paper computes them once, when K enters its KV buffer) and
+ * select with la_select_pooled.
+ *   which  LA_POOL_Q: x = q bf16 [B, H, Lq, d] -> xbar float [B, H, NQ, d];
+ *          LA_POOL_K: x = k bf16 [B, H, Lk, d] -> xbar float [B, H, NK, d].
+ *   A ragged last block is the mean of its valid rows.  Sums in fp32, then one multiply by
+ *   1 / rows: the same values la_select_blocks pools internally, so selecting from them with
+ *   la_select_pooled gives la_select_blocks' result.
+ * A bad `which`, NULL or misaligned pointers are LA_ERR_ARG.  Needs no workspace. */
+enum { LA_POOL_Q = 0, LA_POOL_K = 1 };
+la_status la_pool_blocks(const la_shape* shape, const void* x, int32_t which, float* xbar, void* stream);
+
 /* Block selection from pooled means (Sec. 3.3, selection equation), for block
- * layouts pooled elsewhere (la_prep_q_3d, la_prep_kv_3d).
+ * layouts pooled elsewhere (la_pool_blocks, la_prep_q_3d, la_prep_kv_3d).
  *   shape  the tiled shape; qbar float [B, H, NQ, d], kbar float [B, H, NK, d] (rows
  *          of the M historical blocks are read).
  * Rules, outputs and errors as la_select_blocks / la_select_blocks_topk. */

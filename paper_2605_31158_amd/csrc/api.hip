@@ -97,6 +97,18 @@ static la_status select_pooled_common(const la_shape* shape, const float* qbar, 
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 
+la_status la_pool_blocks(const la_shape* shape, const void* x, int32_t which, float* xbar, void* stream) {
+  Dims dm;
+  la_status st = make_dims(shape, &dm);
+  if (st != LA_OK) return st;
+  if (which != LA_POOL_Q && which != LA_POOL_K) return LA_ERR_ARG;
+  if (!x || !xbar || misaligned(x) || misaligned(xbar)) return LA_ERR_ARG;
+  const int L = which == LA_POOL_Q ? dm.Lq : dm.Lk;
+  const int NB = which == LA_POOL_Q ? dm.NQ : dm.NK;
+  hipError_t e = launch_pool_blocks(dm, x, L, NB, xbar, (hipStream_t)stream);
+  return e == hipSuccess ? LA_OK : LA_ERR_HIP;
+}
+
 la_status la_select_pooled(const la_shape* shape, const float* qbar, const float* kbar, float tau, uint8_t* mask,
                            int32_t* counts, int32_t* idx, void* ws, size_t ws_bytes, void* stream) {
   if (!(tau > 0.0f)) return LA_ERR_ARG;

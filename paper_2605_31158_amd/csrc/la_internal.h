@@ -42,6 +42,8 @@ hipError_t launch_select(const Dims& dm, const void* q, const void* k, float tau
 // Selection from pooled means given by the caller: qbar [BH, NQ, d], kbar [BH, NK, d].
 hipError_t launch_select_pooled(const Dims& dm, const float* qbar, const float* kbar, float tau, int keep_fixed,
                                 uint8_t* mask, int32_t* counts, int32_t* idx, void* ws, hipStream_t st);
+// Block means of x [BH, L, d] in blocks of dm.block rows (ragged last block) into xbar [BH, NB, d].
+hipError_t launch_pool_blocks(const Dims& dm, const void* x, int L, int NB, float* xbar, hipStream_t st);
 hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,
                                hipStream_t st);
 // The attention pass: work plan from the lists, the attention kernel over the plan, merge of

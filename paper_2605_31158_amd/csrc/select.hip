@@ -66,7 +66,8 @@ __device__ inline void wave_block_sum(const uint16_t* __restrict__ base, int row
 }
 
 // ---------------------------------------------------------------------------
-// pooled queries: one wave per query block
+// pooled blocks (the queries here; any [BH, L, D] tensor through launch_pool_blocks): one wave per
+// block
 
 template <int D, int BLOCK>
 __global__ __launch_bounds__(kThreads) void pool_q_kernel(const uint16_t* __restrict__ q,
@@ -490,6 +491,16 @@ hipError_t launch_select_pooled(const Dims& dm, const float* qbar, const float* 
     else launch_score<64, 64, true>(dm, kbar, qbar, scores, st);
   }
   return launch_rows(dm, scores, tau, keep_fixed, mask, counts, idx, st);
+}
+
+hipError_t launch_pool_blocks(const Dims& dm, const void* x, int L, int NB, float* xbar, hipStream_t st) {
+  const dim3 grid(ceil_div(NB, kThreads / 64), dm.BH);
+  const uint16_t* xp = (const uint16_t*)x;
+  if (dm.d == 128 && dm.block == 64) hipLaunchKernelGGL((pool_q_kernel<128, 64>), grid, dim3(kThreads), 0, st, xp, xbar, L, NB);
+  else if (dm.d == 128) hipLaunchKernelGGL((pool_q_kernel<128, 128>), grid, dim3(kThreads), 0, st, xp, xbar, L, NB);
+  else if (dm.block == 64) hipLaunchKernelGGL((pool_q_kernel<64, 64>), grid, dim3(kThreads), 0, st, xp, xbar, L, NB);
+  else hipLaunchKernelGGL((pool_q_kernel<64, 128>), grid, dim3(kThreads), 0, st, xp, xbar, L, NB);
+  return hipGetLastError();
 }
 
 hipError_t launch_mask_to_list(const Dims& dm, const uint8_t* mask, int32_t* counts, int32_t* idx,

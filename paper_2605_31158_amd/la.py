@@ -63,6 +63,7 @@ _SIGNATURES = {
     "la_grid3d_valid": (ctypes.c_int, [_GP, _P, _P]),
     "la_prep_q_3d": (ctypes.c_int, [_GP, _P, _P, _P, _P]),
     "la_prep_kv_3d": (ctypes.c_int, [_GP, _P, _P, ctypes.c_uint32, _P, _P, _P, _P]),
+    "la_pool_blocks": (ctypes.c_int, [_SP, _P, ctypes.c_int32, _P, _P]),
     "la_select_pooled": (ctypes.c_int, [_SP, _P, _P, ctypes.c_float, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_select_pooled_topk": (ctypes.c_int, [_SP, _P, _P, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_fwd_valid": (ctypes.c_int, [_SP, _P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P,
@@ -232,6 +233,24 @@ class BoundCall:
             raise LaError(self._name, st)
 
 
+LA_POOL_Q, LA_POOL_K = 0, 1
+
+
+def pool_blocks(x: torch.Tensor, block: int, which: str, shape: Shape, out: Optional[torch.Tensor] = None):
+    """Block means of q (which="q", -> [B,H,NQ,d]) or k (which="k", -> [B,H,NK,d]) of `shape`, fp32;
+    a ragged last block is the mean of its valid rows."""
+    wcode = {"q": LA_POOL_Q, "k": LA_POOL_K}[which]
+    L = shape.Lq if which == "q" else shape.Lk
+    _check_qkv(which, x, shape.B, shape.H, shape.d)
+    if x.shape[2] != L:
+        raise ValueError(f"{which} must hold {L} tokens")
+    nb = nblocks(L, block)
+    if out is None:
+        out = torch.empty((shape.B, shape.H, nb, shape.d), dtype=torch.float32, device=x.device)
+    _call("la_pool_blocks", ctypes.byref(shape), _ptr(x), ctypes.c_int32(wcode), _ptr(out), _stream(x))
+    return out
+
+
 def bind_attn_steps(q, k, v, counts, idx, block, o, ws, scale: Optional[float] = None, n_text: int = 0,
                     frame_tokens: int = 0, lse: Optional[torch.Tensor] = None):
     """(plan, run, merge) of la_sparse_attn_fwd as BoundCalls on fixed tensors and the current
@@ -253,6 +272,21 @@ def bind_attn_steps(q, k, v, counts, idx, block, o, ws, scale: Optional[float] =
     merge = BoundCall("la_sparse_attn_merge", ctypes.byref(shape), _ptr(o), _ptr(lse), _ptr(ws), nbytes, st,
                       keep=keep)
     return plan, run, merge
+
+
+def bind_select_cached(q, block, tau, kbar, qbar, mask, counts, idx, ws, Lk: int, n_text: int = 0):
+    """(pool Q, select from pooled means) as BoundCalls: the selection of a step whose key means
+    kbar [B,H,NK,d] were pooled earlier (la_pool_blocks); qbar [B,H,NQ,d] is written."""
+    _check_qkv("q", q)
+    B, H, Lq, d = q.shape
+    shape = make_shape(B, H, Lq, Lk, d, block, n_text, 0)
+    st = _stream(q)
+    keep = (q, kbar, qbar, mask, counts, idx, ws, shape)
+    pool = BoundCall("la_pool_blocks", ctypes.byref(shape), _ptr(q), ctypes.c_int32(LA_POOL_Q), _ptr(qbar), st,
+                     keep=keep)
+    sel = BoundCall("la_select_pooled", ctypes.byref(shape), _ptr(qbar), _ptr(kbar), ctypes.c_float(tau), _ptr(mask),
+                    _ptr(counts), _ptr(idx), _ptr(ws), ctypes.c_size_t(ws.numel()), st, keep=keep)
+    return pool, sel
 
 
 def bind_select(q, k, block, tau, mask, counts, idx, ws, n_text: int = 0) -> BoundCall:

@@ -121,6 +121,9 @@ def test_bad_arguments_rejected():
     assert run(ctypes.byref(s), p, p, p, ctypes.c_float(float("nan")), p, None, p, ws, None) == la.LA_ERR_ARG
     assert run(ctypes.byref(s), p, p, p, ctypes.c_float(0), p, None, p, 16, None) == la.LA_ERR_WORKSPACE
     assert lib.la_sparse_attn_merge(ctypes.byref(s), None, None, p, ws, None) == la.LA_ERR_ARG
+    assert lib.la_pool_blocks(ctypes.byref(s), p, 2, p, None) == la.LA_ERR_ARG
+    assert lib.la_pool_blocks(ctypes.byref(s), None, 0, p, None) == la.LA_ERR_ARG
+    assert lib.la_pool_blocks(ctypes.byref(s), p, 1, odd, None) == la.LA_ERR_ARG
     assert lib.la_sparse_attn_merge(ctypes.byref(s), odd, None, p, ws, None) == la.LA_ERR_ARG
 
 

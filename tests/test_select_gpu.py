@@ -132,3 +132,24 @@ def test_select_all_scores_equal(tau):
             for i in range(mask.shape[2]):
                 n = int(mask[b, h, i, :M].sum())
                 assert mask[b, h, i, :n].all(), "ties must keep the lowest block indices"
+
+
+@pytest.mark.parametrize("name", ["tiny", "480p_window"])
+def test_pooled_blocks_and_cached_key_means(name):
+    # la_pool_blocks gives the block means the oracle defines (ragged last block included), and
+    # selecting from cached key means reproduces la_select_blocks exactly
+    wl = WORKLOADS[name]
+    inp = make_inputs(wl)
+    g = to_gpu(inp)
+    shape = la.make_shape(wl.B, wl.H, wl.Lq, wl.Lk, wl.d, wl.block, wl.n_text, 0)
+    qbar = la.pool_blocks(g["q"], wl.block, "q", shape)
+    kbar = la.pool_blocks(g["k"], wl.block, "k", shape)
+    mask_p, counts_p, idx_p = la.select_pooled(shape, qbar, kbar, tau=wl.tau)
+    mask, counts, idx = la.select_blocks(g["q"], g["k"], wl.block, wl.tau, n_text=wl.n_text)
+    torch.cuda.synchronize()
+    assert torch.equal(mask_p, mask) and torch.equal(counts_p, counts)
+    B, H = wl.B, min(wl.H, 2)
+    qb_ref = O.pool_blocks(inp["q"][:, :H], wl.block)
+    kb_ref = O.pool_blocks(inp["k"][:, :H], wl.block)
+    np.testing.assert_allclose(qbar[:, :H].cpu().numpy(), qb_ref, rtol=1e-5, atol=1e-5)
+    np.testing.assert_allclose(kbar[:, :H].cpu().numpy(), kb_ref, rtol=1e-5, atol=1e-5)
