@@ -7,7 +7,7 @@
 //     which chose the same context share a unit.  Its tiles are the 64-key sub-tiles of the
 //     union of its blocks' kept lists, in ascending key order, each tagged with which of the
 //     unit's blocks kept it.
-//   * A planner (three small kernels) computes the grouping keys, every unit's union list and
+//   * A planner (two small kernels) computes the grouping, every unit's union list and
 //     one record per tile (first key, head, unit, ownership) in the concatenated tile sequence
 //     of all units.  One persistent workgroup per CU then takes an equal share of that sequence
 //     (stream-K); a unit cut between two workgroups leaves (O, m, l) partials that attn_combine
@@ -345,26 +345,6 @@ __device__ __forceinline__ void softmax_tile(f32x16* sacc, bf16x8* pb, f32x16* o
 constexpr int kPlanThreads = 256;
 constexpr int kMaxGroupNQ = 1024;   // heads with more query blocks keep the natural order
 
-// Grouping key of every query block: the smallest listed historical block, NK when the list has
-// none (the list is read as a set).  One wave per list.
-__global__ __launch_bounds__(kPlanThreads) void plan_keys_kernel(const int32_t* __restrict__ counts,
-                                                                 const int32_t* __restrict__ idx, int rows, int NK,
-                                                                 int h0, int h1, int32_t* __restrict__ keys) {
-  const int row = blockIdx.x * (kPlanThreads / 64) + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= rows) return;
-  const int n = min(max(counts[row], 0), NK);
-  const int32_t* lst = idx + (size_t)row * NK;
-  int m = NK;
-  for (int a = lane; a < n; a += 64) {
-    const int j = lst[a];
-    if (j >= h0 && j < h1) m = min(m, j);
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) m = min(m, __shfl_xor(m, off));
-  if (lane == 0) keys[row] = m;
-}
-
 __device__ inline int block_excl_scan_i(int x, int* sh, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int incl = x;
@@ -396,11 +376,14 @@ __device__ inline int block_subtiles(int j, int Lk, int block, const int32_t* __
 
 // One workgroup per unit: its query blocks (rank by (key, block index) inside the head) and the
 // union of their lists with ownership bits, expanded into the sub-tiles that hold visible keys.
+// The grouping key of a query block is the first entry of its list past the text blocks when
+// that entry is historical (below h1), NK otherwise: the smallest kept historical block for an
+// ascending list, as the selection writes them, and read in one or a few loads.  Any other
+// list order only changes the grouping.
 __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t* __restrict__ counts,
                                                                   const int32_t* __restrict__ idx,
-                                                                  const int32_t* __restrict__ keys,
                                                                   const int32_t* __restrict__ kvalid, int NQ, int NK,
-                                                                  int Lk, int block, int row_tiles,
+                                                                  int h0, int h1, int Lk, int block, int row_tiles,
                                                                   int32_t* __restrict__ qmap,
                                                                   int32_t* __restrict__ ulist,
                                                                   int32_t* __restrict__ ucount) {
@@ -418,7 +401,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t*
   if (tid < 4) qsel[tid] = -1;
   const bool grouped = NQ <= kMaxGroupNQ;
   if (grouped)
-    for (int i = tid; i < NQ; i += kPlanThreads) skey[i] = keys[(size_t)bh * NQ + i];
+    for (int i = tid; i < NQ; i += kPlanThreads) {
+      const size_t row = (size_t)bh * NQ + i;
+      const int n = min(max(counts[row], 0), NK);
+      const int32_t* lst = idx + row * NK;
+      int key = NK;
+      for (int a = 0; a < n; ++a) {
+        const int j = lst[a];
+        if (j >= h0) {
+          key = j < h1 ? j : NK;
+          break;
+        }
+      }
+      skey[i] = key;
+    }
   __syncthreads();
   if (grouped) {
     for (int i = tid; i < NQ; i += kPlanThreads) {
@@ -934,7 +930,6 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
 struct AttnWs {
   int4* trec;
   int32_t* qmap;
-  int32_t* keys;
   int32_t* ulist;
   int32_t* ucount;
   int32_t* tstart;
@@ -956,8 +951,6 @@ AttnWs attn_ws_layout(const Dims& dm, void* base) {
   off += align256(U * (size_t)dm.NK * (dm.block / KT) * sizeof(int4));
   w.qmap = (int32_t*)(b + off);
   off += align256(U * (size_t)(QR / dm.block) * sizeof(int32_t));
-  w.keys = (int32_t*)(b + off);
-  off += align256((size_t)dm.BH * dm.NQ * sizeof(int32_t));
   w.ulist = (int32_t*)(b + off);
   off += align256(U * (size_t)dm.NK * (dm.block / KT) * sizeof(int32_t));
   w.ucount = (int32_t*)(b + off);
@@ -994,12 +987,9 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
   const int row_tiles = ceil_div(dm.Lq, QR);
   const int U = dm.BH * row_tiles;
   AttnWs w = attn_ws_layout(dm, ws);
-  const int rows = dm.BH * dm.NQ;
-  hipLaunchKernelGGL(plan_keys_kernel, dim3(ceil_div(rows, kPlanThreads / 64)), dim3(kPlanThreads), 0, st, counts,
-                     idx, rows, dm.NK, dm.h0, dm.h1, w.keys);
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
-                     st, counts, idx, w.keys, kvalid, dm.NQ, dm.NK, dm.Lk, dm.block, row_tiles, w.qmap, w.ulist,
-                     w.ucount);
+                     st, counts, idx, kvalid, dm.NQ, dm.NK, dm.h0, dm.h1, dm.Lk, dm.block, row_tiles, w.qmap,
+                     w.ulist, w.ucount);
   hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U, dm.NK,
                      dm.block, row_tiles, w.trec, w.tstart);
   return hipGetLastError();
