@@ -123,7 +123,9 @@ la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k
 
 /* la_sparse_attn_fwd in its three steps, for callers that time or reuse them.
  * The work plan depends only on the lists: units of 256 query rows (query blocks of a
- * head grouped by the first historical block they keep), the union of their lists as
+ * head grouped by the first historical entry of their lists, the first kept historical
+ * block for the ascending lists the selection writes; any order gives the same results),
+ * the union of their lists as
  * 64-key tiles, and the split of all tiles into equal ranges over one persistent
  * workgroup per CU.  It lives in ws.
  *
