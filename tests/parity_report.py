@@ -1,4 +1,4 @@
-"""Parity report over the named workloads (run on a GPU machine; not collected by pytest):
+"""Parity report over the named workloads (needs the GPU; not collected by pytest):
 
     python tests/parity_report.py [workload ...] > report.md
 
