@@ -40,8 +40,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1, help="GPUs (one only: the path runs on one GPU)")
     ap.add_argument("--steps", type=int, default=50, help="timed steps (selection + attention per step)")
     ap.add_argument("--warmup", type=int, default=10, help="untimed steps before the timed ones")
-    ap.add_argument("--workload", default="480p_window",
-                    help="named synthetic workload (1-D: tiny, 480p_window, 480p_memory, 720p, 720p_causal, "
+    ap.add_argument("--workload", default="720p",
+                    help="named synthetic workload, default the largest single-GPU one (1-D: tiny, 480p_window, "
+                         "480p_memory, 720p, 720p_causal, "
                          "480p_long, 480p_long_dense; 3-D: tiny_3d, 480p_3d, 720p_3d)")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the fp64 oracle on the host")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense (every block kept) reference run")
