@@ -293,11 +293,51 @@ def pin_kept_flops():
     assert O.kept_flops(mask, Lq=150, Lk=300, block=64, d=8) == 4 * 8 * (2 * 150 * 300 - 22 * 44)
 
 
+def _band_row(case):
+    """The selection dict ambiguous_blocks reads, for one golden row of scores."""
+    s = np.array(case["scores"], np.float64)[None, None, None]
+    tau, r = case.get("tau"), case.get("r")
+    row = O.select_tau_row(s[0, 0, 0], tau) if tau is not None else O.select_topk_row(s[0, 0, 0], r)
+    return {"scores": s, "part": {"hist": np.array(case["hist"]), "NK": case["NK"]}, "tau": tau,
+            "topk_r": r, "rows": {(0, 0, 0): row}}
+
+
+def pin_ambiguity_band_golden():
+    # every clause of the band on its own, worked by hand (tests/golden/ambiguity_band.json)
+    with open(os.path.join(GOLDEN, "ambiguity_band.json")) as f:
+        g = json.load(f)
+    assert g["tol"] == 1e-4          # the stated tolerance, which is also the band's default
+    for case in g["cases"]:
+        amb = O.ambiguous_blocks(_band_row(case))
+        assert amb[0, 0, 0].tolist() == case["expect_blocks"], case["name"]
+
+
+def pin_ambiguity_band_covers_perturbations():
+    # a flip caused by moving every score by at most 3e-5 (well inside tol = 1e-4) must land
+    # in the band: each golden row, all 3^M moves of its scores by -3e-5, 0 or +3e-5
+    with open(os.path.join(GOLDEN, "ambiguity_band.json")) as f:
+        g = json.load(f)
+    for case in g["cases"]:
+        base = _band_row(case)
+        amb = O.ambiguous_blocks(base, g["tol"])[0, 0, 0]
+        s0 = np.array(case["scores"], np.float64)
+        hist = np.array(case["hist"])
+        keep0 = np.zeros(case["NK"], bool)
+        keep0[hist[base["rows"][(0, 0, 0)]["selected"]]] = True
+        for moves in itertools.product((-3e-5, 0.0, 3e-5), repeat=s0.size):
+            s1 = s0 + np.array(moves)
+            row = O.select_tau_row(s1, case["tau"]) if "tau" in case else O.select_topk_row(s1, case["r"])
+            keep1 = np.zeros(case["NK"], bool)
+            keep1[hist[row["selected"]]] = True
+            assert not ((keep1 != keep0) & ~amb).any(), (case["name"], moves)
+
+
 ALL_PINS = [pin_bf16_decode, pin_partition, pin_pool_closed_form, pin_scores_closed_form,
             pin_softmax_properties, pin_tau_brute_force, pin_topk_brute_force, pin_golden_hand_worked,
             pin_attention_dense_matches_library, pin_attention_sparse_matches_library,
             pin_attention_frame_causal_matches_library, pin_attention_invariants,
-            pin_permutation_invariance, pin_kept_flops]
+            pin_permutation_invariance, pin_kept_flops, pin_ambiguity_band_golden,
+            pin_ambiguity_band_covers_perturbations]
 
 
 @pytest.mark.parametrize("pin", ALL_PINS, ids=[p.__name__ for p in ALL_PINS])

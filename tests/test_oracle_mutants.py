@@ -30,6 +30,20 @@ MUTANTS = {
     "top-k off by one": ("kstar = max(0, min(kstar, M))", "kstar = max(0, min(kstar + 1, M))"),
     "bf16 decode shift": ("astype(np.uint32) << 16", "astype(np.uint32) << 15"),
     "kept flops drops factor": ("return int(4 * d *", "return int(2 * d *"),
+    # the ambiguity band (which mask differences the GPU comparison forgives)
+    "band: tie clause needs three": ("if near.sum() > 1:", "if near.sum() > 2:"),
+    "band: tie clause dropped": ("                flag |= near\n", "                pass\n"),
+    "band: crossing margin sign": ('if sel["tau"] - before <= tol:', 'if before - sel["tau"] <= tol:'),
+    "band: crossing margin from C_k*": ("before = cum[kstar - 2] if kstar >= 2 else 0.0", "before = cum[kstar - 1]"),
+    "band: first-dropped clause flags the last kept": ("flag[order[kstar]] = True", "flag[order[kstar - 1]] = True"),
+    "band: first-dropped margin from C_k*-1": ('cum[kstar - 1] - sel["tau"] <= tol', 'cum[kstar - 2] - sel["tau"] <= tol'),
+    "band: top-k gap test inverted": ("if lo_kept - hi_dropped <= tol:", "if lo_kept - hi_dropped > tol:"),
+    "band: top-k window without tol": ("flag |= (sr >= hi_dropped - tol) & (sr <= lo_kept + tol)",
+                                       "flag |= (sr >= hi_dropped) & (sr <= lo_kept)"),
+    "band: candidates not mapped to blocks": ("amb[b, h, i, hist[flag]] = True", "amb[b, h, i, np.nonzero(flag)[0]] = True"),
+    "band: tolerance 1e-3": ("def ambiguous_blocks(sel: Dict[str, object], tol: float = 1e-4)",
+                             "def ambiguous_blocks(sel: Dict[str, object], tol: float = 1e-3)"),
+    "band: tau >= 1 not exempt": ('            if sel["tau"] >= 1.0:\n                continue\n', ""),
 }
 
 
