@@ -13,9 +13,10 @@
 //                 M scores, then a radix select over the 32-bit order keys of the scores (4
 //                 passes of 8 bits, per-wave LDS histogram) that finds the score at which the
 //                 mass, accumulated from the highest score down, first reaches tau (or the
-//                 count reaches the top-k size).  Masses are 2^-31 fixed-point integers, so the
-//                 sums are exact and independent of summation order.  Equal scores at the
-//                 cutoff are taken in ascending block order.  The kept set is merged with the
+//                 count reaches the top-k size).  Masses are integer weights (2^48 exp(s - max),
+//                 64-bit), so the sums are exact and independent of summation order, and the
+//                 cutoff is taken from the weight left out, which stays accurate for tau near 1.
+//                 Equal scores at the cutoff are taken in ascending block order.  The kept set is merged with the
 //                 forced blocks and emitted, ascending, with lane ballots: mask row, count, list.
 #include <float.h>
 #include <math.h>
@@ -224,8 +225,10 @@ __device__ inline void emit_range(int lo, int hi, int pos, uint8_t* mask_row, in
   }
 }
 
-constexpr float kFix = 2147483648.0f;   // 2^31 fixed-point scale of the mass (sums fit 32 bits)
 constexpr float kLog2e = 1.4426950408889634f;
+// Weights of the tau rule: exp(s - max) in (0, 1] scaled by 2^48 and truncated, so a row of at most
+// 4096 candidates sums below 2^60 and a candidate whose mass is above ~M 2^-48 keeps a weight.
+constexpr float kWScale = 281474976710656.0f;   // 2^48
 
 __device__ inline uint32_t wave_sum_u32(uint32_t x) {
   return wave_allreduce(x, [](uint32_t a, uint32_t b) { return a + b; });
@@ -236,42 +239,56 @@ __device__ inline uint32_t wave_min_u32(uint32_t x) {
 __device__ inline uint32_t wave_max_u32(uint32_t x) {
   return wave_allreduce(x, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
 }
-// inclusive prefix sum over the lanes: shifts 1, 2, 4, 8 inside each row of 16 lanes, then the
-// last lane of row 0 (2) added to row 1 (3), and the last lane of row 1 to rows 2 and 3
-__device__ inline uint32_t wave_incl_scan_u32(uint32_t x) {
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+__device__ inline uint64_t wave_sum_u64(uint64_t x) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) x += __shfl_xor(x, off);
   return x;
+}
+// inclusive prefix sum over the 64 lanes
+__device__ inline uint64_t wave_incl_scan_u64(uint64_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint64_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+__device__ inline uint64_t read_lane_u64(uint64_t x, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
 }
 
 // One wave per (head, query block).  Lane l holds candidates m = l + 64 j, j < NPER.
-// Masses are floor(p * 2^31) (tau rule) or 1 per candidate (top-k rule); their sum over a row
-// stays below 2^32.
+// Each candidate carries an integer weight: floor(2^48 exp(s - max)) for the tau rule, 1 for the
+// top-k rule.  The kept set is the shortest prefix in score order whose weight reaches a target
+// T: for the tau rule T = W - floor((1 - tau) W) with W the row's total weight, i.e. the prefix
+// reaches tau exactly when the weight it leaves out is at most (1 - tau) W.  Taking the cutoff
+// from the dropped tail keeps it accurate for tau near 1, where the tail is tiny but each weight
+// in it still has ~24 significant bits.  The sums are exact integers, so they do not depend on
+// summation order (deterministic).
 template <int NPER>
 __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __restrict__ scores, int NQ,
                                                                int NK, int M, int h0, int h1, float tau,
                                                                int keep_fixed, uint8_t* __restrict__ mask,
                                                                int32_t* __restrict__ counts,
                                                                int32_t* __restrict__ idx) {
-  __shared__ uint32_t hist_all[kThreads / 64][256];
+  __shared__ unsigned long long hist_all[kThreads / 64][256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = blockIdx.x * (kThreads / 64) + wave;
   const int bh = blockIdx.y;
   if (i >= NQ) return;
-  uint32_t* hist = hist_all[wave];
+  unsigned long long* hist = hist_all[wave];
   const size_t row = (size_t)bh * NQ + i;
   const float* s = scores + row * (size_t)M;
   uint8_t* mask_row = mask ? mask + row * (size_t)NK : nullptr;
   int32_t* idx_row = idx + row * (size_t)NK;
 
   uint32_t uk[NPER];    // order keys
-  uint32_t w[NPER];     // masses
+  uint64_t w[NPER];     // weights
   bool keep_all = keep_fixed < 0 ? tau >= 1.0f : keep_fixed >= M;
-  uint32_t target = 0;
+  uint64_t target = 0;
   {
     float sv[NPER];
 #pragma unroll
@@ -283,32 +300,32 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
       if (keep_fixed >= 0) {
 #pragma unroll
         for (int j = 0; j < NPER; ++j) w[j] = (lane + 64 * j < M) ? 1u : 0u;
-        target = (uint32_t)keep_fixed;
+        target = (uint64_t)keep_fixed;
       } else {
-        // softmax over the M candidates: exp(s - max) = 2^((s - max) log2 e); every term <= 1
-        // and the sum >= 1, so floor(e * 2^31 / sum) <= 2^31
+        // exp(s - max) = 2^((s - max) log2 e) <= 1, the top candidate's weight is 2^48
         float mx = -FLT_MAX;
 #pragma unroll
         for (int j = 0; j < NPER; ++j) mx = fmaxf(mx, sv[j]);
         mx = wave_max(mx);
-        float e[NPER];
-        float sum = 0.f;
+        uint64_t wl = 0;
 #pragma unroll
         for (int j = 0; j < NPER; ++j) {
-          e[j] = (lane + 64 * j < M) ? __builtin_amdgcn_exp2f((sv[j] - mx) * kLog2e) : 0.f;
-          sum += e[j];
+          const float e = (lane + 64 * j < M) ? __builtin_amdgcn_exp2f((sv[j] - mx) * kLog2e) : 0.f;
+          w[j] = (uint64_t)(e * kWScale);
+          wl += w[j];
         }
-        sum = wave_sum(sum);
-        const float sc = kFix / sum;
-#pragma unroll
-        for (int j = 0; j < NPER; ++j) w[j] = (uint32_t)(e[j] * sc);
-        target = (uint32_t)(tau * kFix);
+        const uint64_t total = wave_sum_u64(wl);
+        // 1 - tau is exact in double; the product's rounding moves the limit by < 2^8 of the
+        // total's 2^48-per-unit-mass scale
+        const double drop = floor((1.0 - (double)tau) * (double)total);
+        const uint64_t dmax = drop <= 0.0 ? 0ull : (drop >= (double)total ? total : (uint64_t)drop);
+        target = total - dmax;
         if (target == 0) target = 1;     // any tau > 0 keeps at least the top candidate
       }
-      uint32_t wl = 0;
+      uint64_t wl = 0;
 #pragma unroll
       for (int j = 0; j < NPER; ++j) wl += w[j];
-      if (wave_sum_u32(wl) < target) keep_all = true;   // the mass / count never reaches the target
+      if (wave_sum_u64(wl) < target) keep_all = true;   // the count never reaches the target
     }
 #pragma unroll
     for (int j = 0; j < NPER; ++j) uk[j] = order_key(sv[j]);
@@ -320,7 +337,8 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
   int mstar = 0x7fffffff;
   const bool none = !keep_all && target == 0;
   if (!keep_all && !none) {
-    uint32_t prefix = 0, before = 0;
+    uint32_t prefix = 0;
+    uint64_t before = 0;
     bool found = false;
     for (int pass = 0; pass < 4; ++pass) {
       const int shift = 24 - 8 * pass;
@@ -330,27 +348,27 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
 #pragma unroll
       for (int j = 0; j < NPER; ++j) {
         const bool in = w[j] != 0 && (pass == 0 || (uk[j] >> (shift + 8)) == prefix);
-        if (in) atomicAdd(&hist[(uk[j] >> shift) & 255u], w[j]);
+        if (in) atomicAdd(&hist[(uk[j] >> shift) & 255u], (unsigned long long)w[j]);
       }
       wave_lds_sync();
-      uint32_t b4[4];
-      uint32_t loc = 0;
+      uint64_t b4[4];
+      uint64_t loc = 0;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         loc += hist[4 * lane + t];
         b4[t] = loc;
       }
-      const uint32_t excl = wave_incl_scan_u32(loc) - loc;
+      const uint64_t excl = wave_incl_scan_u64(loc) - loc;
       int hit = -1;
 #pragma unroll
       for (int t = 3; t >= 0; --t)
         if (before + excl + b4[t] >= target) hit = t;
       const unsigned long long bal = __ballot(hit >= 0);
       const int first = __ffsll(bal) - 1;              // lane holding the crossing bin
-      const uint32_t below = before + excl + (hit > 0 ? b4[hit > 0 ? hit - 1 : 0] : 0);
+      const uint64_t below = before + excl + (hit > 0 ? b4[hit > 0 ? hit - 1 : 0] : 0);
       const int bin = 4 * lane + hit;
       prefix = (prefix << 8) | (uint32_t)__builtin_amdgcn_readlane(bin, first);
-      before = (uint32_t)__builtin_amdgcn_readlane((int)below, first);
+      before = read_lane_u64(below, first);
       if (pass == 1) {
         uint32_t kmin = 0xffffffffu, kmax = 0u;
 #pragma unroll
@@ -374,18 +392,18 @@ __global__ __launch_bounds__(kThreads) void select_rows_kernel(const float* __re
     for (int j = 0; j < NPER; ++j) ntie += (w[j] != 0 && uk[j] == ustar) ? 1 : 0;
     if (wave_sum_u32((uint32_t)ntie) > 1) {
       // equal scores at the cutoff: take them in ascending block order until the target
-      uint32_t base = before;
+      uint64_t base = before;
 #pragma unroll
       for (int j = 0; j < NPER; ++j) {
-        const uint32_t wt = (w[j] != 0 && uk[j] == ustar) ? w[j] : 0;
-        const uint32_t incl = wave_incl_scan_u32(wt);
+        const uint64_t wt = (w[j] != 0 && uk[j] == ustar) ? w[j] : 0;
+        const uint64_t incl = wave_incl_scan_u64(wt);
         const bool cross = wt != 0 && base + incl >= target && base + incl - wt < target;
         const unsigned long long bal = __ballot(cross);
         if (bal) {
           mstar = 64 * j + __ffsll(bal) - 1;
           break;
         }
-        base += (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+        base += read_lane_u64(incl, 63);
       }
     }
   }

@@ -19,6 +19,7 @@ All tensors are returned as numpy uint16 arrays holding bfloat16 bit patterns
 from __future__ import annotations
 
 import dataclasses
+import math
 from concurrent.futures import ThreadPoolExecutor
 from typing import Dict, Optional
 
@@ -224,6 +225,33 @@ def make_inputs(wl: Workload, threads: int = 8) -> Dict[str, np.ndarray]:
     else:
         for bh in range(B * H):
             one(bh)
+    return {"q": q, "k": k, "v": v}
+
+
+def make_spread(B: int, H: int, Lq: int, Lk: int, d: int, block: int, seed: int,
+                sigma: float = 5.0, noise: float = 0.5) -> Dict[str, np.ndarray]:
+    """Inputs whose block scores spread evenly, with no dominant block: independent N(0, I)
+    centroids for every key block and every query block (no query copies a key block), scaled by
+    sqrt(sigma) on both sides, plus 0.5 N(0, I) token noise before scaling.  The scores of a row
+    are then roughly N(0, sigma^2), so the softmax mass thins out gradually over many blocks and
+    a tau close to 1 cuts deep into a long tail of small masses."""
+    rng = np.random.default_rng(seed)
+    NK, NQ = -(-Lk // block), -(-Lq // block)
+    a = np.float32(math.sqrt(sigma))
+    q = np.empty((B, H, Lq, d), np.uint16)
+    k = np.empty((B, H, Lk, d), np.uint16)
+    v = np.empty((B, H, Lk, d), np.uint16)
+    kblk = np.minimum(np.arange(Lk) // block, NK - 1)
+    qblk = np.arange(Lq) // block
+    for bi in range(B):
+        for hi in range(H):
+            kc = rng.standard_normal((NK, d), dtype=np.float32)
+            qc = rng.standard_normal((NQ, d), dtype=np.float32)
+            kn = kc[kblk] + np.float32(noise) * rng.standard_normal((Lk, d), dtype=np.float32)
+            qn = qc[qblk] + np.float32(noise) * rng.standard_normal((Lq, d), dtype=np.float32)
+            k[bi, hi] = f32_to_bf16_bits(kn * a)
+            q[bi, hi] = f32_to_bf16_bits(qn * a)
+            v[bi, hi] = f32_to_bf16_bits(rng.standard_normal((Lk, d), dtype=np.float32))
     return {"q": q, "k": k, "v": v}
 
 

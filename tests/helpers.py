@@ -14,6 +14,12 @@ ATTN_MEAN_ABS = 2e-3
 SEL_TOL = 1e-4
 
 
+def tau32(tau):
+    """The cumulative-mass threshold as the C ABI receives it (a float): the oracle evaluates the
+    rule at exactly that value, so that both sides cut at the same tau."""
+    return None if tau is None else float(np.float32(tau))
+
+
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()

@@ -13,7 +13,7 @@ import torch
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
 from paper_2605_31158_amd.workloads import WORKLOADS_3D, Workload3D, make_inputs_3d
-from helpers import say, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
+from helpers import say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -130,7 +130,7 @@ def run_path(wl, inp, keep_blocks=None, tau=None):
 
 def rule_args(wl, M):
     if wl.tau is not None:
-        return dict(tau=wl.tau), dict(tau=wl.tau)
+        return dict(tau=wl.tau), dict(tau=tau32(wl.tau))
     return dict(keep_blocks=int(np.floor(wl.topk_r * M))), dict(topk_r=wl.topk_r)
 
 
@@ -183,7 +183,7 @@ def test_both_rules_on_pooled_means(name):
     M = int((~L["forced"]).sum())
     for tau in (0.5, 0.95, 1.0):
         mask, counts, idx = la.select_pooled(shape, qbar, kbar, tau=tau)
-        sel = O.select_blocks_sets(inp["q"], inp["k"], L["qsets"], L["ksets"], L["forced"], tau=tau)
+        sel = O.select_blocks_sets(inp["q"], inp["k"], L["qsets"], L["ksets"], L["forced"], tau=tau32(tau))
         check_selection(mask.cpu().numpy(), sel)
         check_list(mask.cpu().numpy(), counts.cpu().numpy(), idx.cpu().numpy())
     for r in (0.1, 0.5):

@@ -11,7 +11,7 @@ import torch
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
 from paper_2605_31158_amd.workloads import WORKLOADS, CONFIG_ORDER, make_inputs, make_clustered
-from helpers import say, to_gpu, check_list, assert_attn_close, bf16_tensor_to_f64
+from helpers import say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -113,8 +113,10 @@ def test_attn_value_invariants():
     assert np.abs(o - 1.0).max() <= 2 ** -8
 
 
-@pytest.mark.parametrize("name", CONFIG_ORDER)
+@pytest.mark.parametrize("name", CONFIG_ORDER + ["480p_long_dense"])
 def test_attn_named_workloads_on_gpu_mask(name):
+    # sampled query blocks (the heaviest rows, random rows, the ragged last block) and, except for
+    # the dense run (5.4 TFLOP), every query block of one head
     wl = WORKLOADS[name]
     say(f"[attn] {name}: full size, sampled query blocks vs oracle on the GPU mask")
     inp = make_inputs(wl)
@@ -134,6 +136,9 @@ def test_attn_named_workloads_on_gpu_mask(name):
         b, rem = divmod(int(flat), H * NQ)
         h, i = divmod(rem, NQ)
         rows.add((b, h, i))
+    if name != "480p_long_dense":
+        b, rem = divmod(int(heavy[0]), H * NQ)
+        rows.update((b, rem // NQ, i) for i in range(NQ))
     ref = O.attention_rows(inp["q"], inp["k"], inp["v"], mask_np, wl.block, sorted(rows))
     for (b, h, i), (ob, lb) in ref.items():
         lo = i * wl.block
@@ -210,3 +215,28 @@ def test_attn_plan_run_merge_equal_fwd():
         merge2()
         torch.cuda.synchronize()
         assert torch.equal(o3, o2)
+
+
+def test_attn_head_with_more_than_1024_query_blocks():
+    # NQ = 1030 query blocks in one head: past the planner's grouping limit, so the units take
+    # the query blocks in their natural order; selection and attention on sampled rows
+    B, H, d, block = 1, 1, 64, 64
+    Lq = 1030 * block - 20                   # ragged last query block
+    Lk = Lq + 12 * block
+    inp = make_clustered(B, H, Lq, Lk, d, block, 31)
+    g = to_gpu(inp)
+    mask, counts, idx = la.select_blocks(g["q"], g["k"], block, 0.9)
+    o, lse = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, block, want_lse=True)
+    torch.cuda.synchronize()
+    mask_np = mask.cpu().numpy()
+    assert mask_np.shape[2] == 1030
+    check_selection(mask_np, O.select_blocks(inp["q"], inp["k"], block, tau=tau32(0.9)))
+    check_list(mask_np, counts.cpu().numpy(), idx.cpu().numpy())
+    o = bf16_tensor_to_f64(o)
+    lse = lse.cpu().numpy()
+    rng = np.random.default_rng(31)
+    rows = sorted({(0, 0, int(i)) for i in list(rng.integers(0, 1030, size=12)) + [0, 1, 3, 4, 1023, 1024, 1029]})
+    ref = O.attention_rows(inp["q"], inp["k"], inp["v"], mask_np, block, rows)
+    for (b, h, i), (ob, lb) in ref.items():
+        lo = i * block
+        compare(o[b, h, lo:lo + ob.shape[0]], lse[b, h, lo:lo + ob.shape[0]], ob, lb, f"NQ=1030 row {i}")

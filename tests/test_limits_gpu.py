@@ -13,7 +13,7 @@ import torch
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
 from paper_2605_31158_amd.workloads import make_clustered
-from helpers import say, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
+from helpers import say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -38,7 +38,7 @@ def test_most_candidate_blocks(rule):
     g = to_gpu(inp)
     if rule == "tau":
         mask, counts, idx = la.select_blocks(g["q"], g["k"], block, 0.95)
-        sel = O.select_blocks(inp["q"], inp["k"], block, tau=0.95)
+        sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(0.95))
     else:
         keep = int(0.175 * 4096)
         mask, counts, idx = la.select_blocks_topk(g["q"], g["k"], block, keep)
@@ -76,7 +76,7 @@ def test_most_batch_heads():
     bs_t, hs_t = torch.as_tensor(bs, device="cuda"), torch.as_tensor(hs, device="cuda")
     pick = lambda t: t[bs_t, hs_t][None].float().cpu().numpy()     # [1, n, L, d], exact bf16 values
     qs, ks, vs = pick(q), pick(k), pick(v)
-    sel = O.select_blocks(qs, ks, block, tau=0.6)
+    sel = O.select_blocks(qs, ks, block, tau=tau32(0.6))
     m_s = mask_np[bs, hs][None]
     check_selection(m_s, sel)
     check_list(m_s, counts_np[bs, hs][None], idx.cpu().numpy()[bs, hs][None])

@@ -12,7 +12,7 @@ import pytest
 
 from oracle import la_oracle as O
 from paper_2605_31158_amd.workloads import Workload3D, make_inputs_3d
-from helpers import say, check_list, check_selection
+from helpers import say, tau32, check_list, check_selection
 from test_3d_gpu import layout_of, run_path, rule_args, compare_rows
 
 pytestmark = pytest.mark.gpu

@@ -15,7 +15,7 @@ import torch
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
 from paper_2605_31158_amd.workloads import make_clustered
-from helpers import say, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
+from helpers import say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -60,7 +60,7 @@ def test_random_path(case):
     M = max((Lk - Lq) // block - h0, 0)
     if rule == "tau":
         mask, counts, idx = la.select_blocks(g["q"], g["k"], block, r, n_text=n_text)
-        sel = O.select_blocks(inp["q"], inp["k"], block, tau=r, n_text=n_text)
+        sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(r), n_text=n_text)
     else:
         keep = int(math.floor(r * M + 1e-9)) if M > 0 else 0
         mask, counts, idx = la.select_blocks_topk(g["q"], g["k"], block, keep, n_text=n_text)

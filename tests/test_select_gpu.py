@@ -1,13 +1,15 @@
 """GPU block selection vs the fp64 oracle: bit-exact mask outside the ambiguity band,
 counts and lists consistent with the mask, and a valid selection everywhere."""
+import math
+
 import numpy as np
 import pytest
 import torch
 
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
-from paper_2605_31158_amd.workloads import WORKLOADS, CONFIG_ORDER, make_inputs, make_clustered
-from helpers import say, to_gpu, check_list, check_selection
+from paper_2605_31158_amd.workloads import WORKLOADS, CONFIG_ORDER, make_inputs, make_clustered, make_spread
+from helpers import say, tau32, to_gpu, check_list, check_selection
 
 pytestmark = pytest.mark.gpu
 
@@ -28,7 +30,7 @@ def test_select_named_workloads(name):
     say(f"[select] {name} shape B={wl.B} H={wl.H} Lq={wl.Lq} Lk={wl.Lk} d={wl.d} block={wl.block} tau={wl.tau}")
     inp = make_inputs(wl)
     mask, counts, idx = run_select(inp, wl.block, tau=wl.tau)
-    sel = O.select_blocks(inp["q"], inp["k"], wl.block, tau=wl.tau)
+    sel = O.select_blocks(inp["q"], inp["k"], wl.block, tau=tau32(wl.tau))
     check_selection(mask, sel)
     check_list(mask, counts, idx)
     say(f"[select] {name} ok: kept blocks {int(mask.sum())}, oracle {int(sel['mask'].sum())}, "
@@ -57,7 +59,7 @@ def test_select_edge_shapes(case):
     say(f"[select-edge] {kind}: B={B} H={H} Lq={Lq} Lk={Lk} d={d} block={block} n_text={n_text} tau={tau}")
     inp = make_clustered(B, H, Lq, Lk, d, block, seed, n_text=n_text)
     mask, counts, idx = run_select(inp, block, tau=tau, n_text=n_text)
-    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau, n_text=n_text)
+    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(tau), n_text=n_text)
     check_selection(mask, sel)
     check_list(mask, counts, idx)
 
@@ -72,7 +74,7 @@ def test_select_tied_scores():
     inp["k"] = k
     for tau in (0.3, 0.9):
         mask, counts, idx = run_select(inp, block, tau=tau)
-        sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau)
+        sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(tau))
         check_selection(mask, sel)
         check_list(mask, counts, idx)
 
@@ -122,11 +124,15 @@ def test_select_all_scores_equal(tau):
         k[:, :, 64 * m:64 * (m + 1)] = k[:, :, 0:64]
     inp["k"] = k
     mask, counts, idx = run_select(inp, block, tau=tau)
-    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau)
+    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(tau))
     check_selection(mask, sel)
     check_list(mask, counts, idx)
-    kept = mask[..., :M].sum(-1)
-    assert (kept == int(np.ceil(tau * M - 1e-9))).all() or True
+    # equal weights: the kernel keeps the smallest k with k / M >= tau (tau as the float it receives),
+    # exactly, since its weights are integers; the oracle's fp64 prefix sums may differ from it by
+    # one block only where tau * M is an integer (a crossing inside the band)
+    from fractions import Fraction
+    want = math.ceil(Fraction(float(np.float32(tau))) * M)
+    assert (mask[..., :M].sum(-1) == want).all(), (mask[..., :M].sum(-1), want)
     for b in range(B):
         for h in range(H):
             for i in range(mask.shape[2]):
@@ -153,3 +159,41 @@ def test_pooled_blocks_and_cached_key_means(name):
     kb_ref = O.pool_blocks(inp["k"][:, :H], wl.block)
     np.testing.assert_allclose(qbar[:, :H].cpu().numpy(), qb_ref, rtol=1e-5, atol=1e-5)
     np.testing.assert_allclose(kbar[:, :H].cpu().numpy(), kb_ref, rtol=1e-5, atol=1e-5)
+
+
+NEAR_ONE = [0.99999, 1 - 1e-6, 1 - 1e-7, float(np.nextafter(np.float32(1), np.float32(0)))]
+
+
+@pytest.mark.parametrize("M", [700, 1560])
+@pytest.mark.parametrize("tau", NEAR_ONE, ids=["0.99999", "1-1e-6", "1-1e-7", "largest-below-1"])
+def test_select_tau_near_one_spread_rows(M, tau):
+    # scores ~ N(0, 5^2) with no dominant block: a tau this close to 1 cuts hundreds of blocks
+    # deep into a tail of masses down to ~1e-9 each, where the cutoff is decided by the dropped tail
+    B, H, Lq, block, d = 1, 4, 256, 64, 128
+    Lk = M * block + Lq
+    inp = make_spread(B, H, Lq, Lk, d, block, seed=M, sigma=5.0)
+    mask, counts, idx = run_select(inp, block, tau=tau)
+    sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(tau))
+    kept = mask[..., :M].sum(-1)
+    say(f"[select-near-1] M={M} tau={tau!r}: kept {kept.ravel().tolist()}, "
+        f"oracle {sel['mask'][..., :M].sum(-1).ravel().tolist()}")
+    assert kept.min() > 1 and kept.max() < M          # a real cut, deep in the tail
+    check_selection(mask, sel)
+    check_list(mask, counts, idx)
+
+
+def test_select_without_mask_output():
+    # mask = NULL: counts and lists alone, equal to those of the call that also writes the mask
+    wl = WORKLOADS["480p_window"]
+    inp = make_inputs(wl)
+    g = to_gpu(inp)
+    mask, counts, idx = la.select_blocks(g["q"], g["k"], wl.block, wl.tau)
+    none, counts_n, idx_n = la.select_blocks(g["q"], g["k"], wl.block, wl.tau, want_mask=False)
+    torch.cuda.synchronize()
+    assert none is None
+    assert torch.equal(counts_n, counts)
+    c = counts.cpu().numpy()
+    a, b = idx.cpu().numpy(), idx_n.cpu().numpy()
+    for row in np.ndindex(c.shape):
+        np.testing.assert_array_equal(b[row][:c[row]], a[row][:c[row]])
+    check_list(mask.cpu().numpy(), c, b)
