@@ -193,8 +193,6 @@ struct WaveCtx {
 
 // Scheduling-group masks of __builtin_amdgcn_sched_group_barrier.
 constexpr int kSgMfma = 0x008;
-constexpr int kSgValu = 0x002 | 0x400;   // VALU and transcendental
-constexpr int kSgVmemRead = 0x020;
 constexpr int kSgDsRead = 0x100;
 
 // S^T = K Q^T for one 64-key tile: two 32x32 accumulators (keys 0..31, 32..63).  The K operand

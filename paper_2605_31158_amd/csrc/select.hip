@@ -203,11 +203,6 @@ __device__ inline float wave_max(float x) {
     return __builtin_bit_cast(uint32_t, fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
   }));
 }
-__device__ inline float wave_sum(float x) {
-  return __builtin_bit_cast(float, wave_allreduce(__builtin_bit_cast(uint32_t, x), [](uint32_t a, uint32_t b) {
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
-  }));
-}
 __device__ inline uint64_t lanes_below(int lane) { return lane == 0 ? 0ull : (~0ull >> (64 - lane)); }
 
 // All LDS operations this wave issued have completed before the next one starts.
