@@ -96,6 +96,24 @@ la_status la_select_blocks(const la_shape* shape, const void* q, const void* k, 
                            uint8_t* mask, int32_t* counts, int32_t* idx,
                            void* ws, size_t ws_bytes, void* stream);
 
+/* la_select_blocks with no workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  The scratch it needs (pooled queries and the score matrix,
+ * la_workspace_bytes' selection part) is a device array of LA_NOALLOC_SCRATCH_BYTES
+ * inside the library, one per GPU, held from the library's load until the process ends;
+ * the call itself allocates nothing.
+ *   Arguments, rule, outputs and errors as la_select_blocks; shapes whose selection
+ *   scratch exceeds LA_NOALLOC_SCRATCH_BYTES (4 B * B*H*NQ*(d + M), rounded up to 256 B per
+ *   part) return LA_ERR_WORKSPACE.  Every benchmark shape fits (at most 10.6 MB).
+ *   The scratch belongs to the current device (hipGetDevice), which must be the device
+ *   of q, k and the stream.  All calls on one GPU share it: calls that may overlap on one
+ *   GPU (concurrent streams, or threads enqueueing at once) race; calls ordered on one
+ *   stream do not.  Nothing carries over between calls (each call writes every scratch
+ *   byte it reads). */
+#define LA_NOALLOC_SCRATCH_BYTES (16u << 20)
+la_status la_select_blocks_noalloc(const la_shape* shape, const void* q, const void* k, float tau,
+                                   uint8_t* mask, int32_t* counts, int32_t* idx, void* stream);
+
 /* The paper's Top-floor(rM) rule (Sec. 3.3, selection equation): keep the
  * keep_blocks = floor(r*M) highest-scoring historical blocks, computed by the
  * caller and clamped to [0, M] here (0 keeps only the forced blocks).  Same

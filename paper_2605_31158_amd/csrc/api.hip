@@ -2,6 +2,8 @@
 // sizing and kernel launches.  Nothing here allocates device memory.
 #include <math.h>
 
+#include <mutex>
+
 #include "la_internal.h"
 
 namespace la {
@@ -75,6 +77,48 @@ la_status la_select_blocks(const la_shape* shape, const void* q, const void* k, 
                            void* stream) {
   if (!(tau > 0.0f)) return LA_ERR_ARG;   // also rejects NaN
   return select_common(shape, q, k, tau, -1, mask, counts, idx, ws, ws_bytes, stream);
+}
+
+// Scratch of la_select_blocks_noalloc (pooled queries and scores of one call): a device array
+// the code object carries, so the call needs no allocation.  Each device holds its own copy, at
+// its own address, from module load until the process ends.  In host code `scratch` names a
+// host-side stand-in; the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[LA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up on the first call on that device (with
+// it current) and kept.
+la_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return LA_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LA_OK;
+}
+}  // namespace
+
+la_status la_select_blocks_noalloc(const la_shape* shape, const void* q, const void* k, float tau,
+                                   uint8_t* mask, int32_t* counts, int32_t* idx, void* stream) {
+  if (!(tau > 0.0f)) return LA_ERR_ARG;
+  Dims dm;
+  la_status st = make_dims(shape, &dm);
+  if (st != LA_OK) return st;
+  if (!q || !k || !counts || !idx || misaligned(q) || misaligned(k)) return LA_ERR_ARG;
+  if (select_ws_bytes(dm) > (size_t)LA_NOALLOC_SCRATCH_BYTES) return LA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  st = scratch_of_current_device(&ws);
+  if (st != LA_OK) return st;
+  // every scratch byte the kernels read is written earlier in the same call: nothing to clear
+  return select_common(shape, q, k, tau, -1, mask, counts, idx, ws, LA_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 la_status la_select_blocks_topk(const la_shape* shape, const void* q, const void* k, int32_t keep_blocks,

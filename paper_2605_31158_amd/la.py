@@ -54,6 +54,7 @@ _SIGNATURES = {
     "la_workspace_bytes": (ctypes.c_size_t, [_SP]),
     "la_select_blocks": (ctypes.c_int, [_SP, _P, _P, ctypes.c_float, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_select_blocks_topk": (ctypes.c_int, [_SP, _P, _P, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_select_blocks_noalloc": (ctypes.c_int, [_SP, _P, _P, ctypes.c_float, _P, _P, _P, _P]),
     "la_sparse_attn_fwd": (ctypes.c_int, [_SP, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_plan": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_run": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -158,6 +159,18 @@ def select_blocks_topk(q: torch.Tensor, k: torch.Tensor, block: int, keep_blocks
                        out: Optional[Tuple[torch.Tensor, torch.Tensor, torch.Tensor]] = None):
     """Top-keep_blocks selection (the paper's Top-floor(rM) rule with keep_blocks = floor(r*M))."""
     return _select("la_select_blocks_topk", ctypes.c_int32(keep_blocks), q, k, block, n_text, want_mask, ws, out)
+
+
+def select_blocks_noalloc(q: torch.Tensor, k: torch.Tensor, block: int, tau: float, mask: Optional[torch.Tensor],
+                          counts: torch.Tensor, idx: torch.Tensor, n_text: int = 0):
+    """la_select_blocks_noalloc into the caller's outputs (mask may be None): the library's own
+    scratch instead of a workspace, nothing allocated by the call or here."""
+    _check_qkv("q", q)
+    B, H, Lq, d = q.shape
+    _check_qkv("k", k, B, H, d)
+    shape = make_shape(B, H, Lq, k.shape[2], d, block, n_text, 0)
+    _call("la_select_blocks_noalloc", ctypes.byref(shape), _ptr(q), _ptr(k), ctypes.c_float(tau), _ptr(mask),
+          _ptr(counts), _ptr(idx), _stream(q))
 
 
 def _select(fn, rule_arg, q, k, block, n_text, want_mask, ws, out):

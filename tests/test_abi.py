@@ -127,6 +127,27 @@ def test_bad_arguments_rejected():
     assert lib.la_sparse_attn_merge(ctypes.byref(s), odd, None, p, ws, None) == la.LA_ERR_ARG
 
 
+@cpu_only
+def test_noalloc_selection_rejects_before_any_gpu_call():
+    # bad arguments, bad shapes and shapes whose selection scratch exceeds the library's array
+    # (4 B x B*H*NQ*(d + M) > 16 MiB) are refused before the scratch is looked up
+    lib = la.lib()
+    p = ctypes.c_void_p(4096)
+    odd = ctypes.c_void_p(4098)
+    na = lib.la_select_blocks_noalloc
+    s = la.make_shape(1, 2, 256, 1024, 64, 64)
+    assert na(ctypes.byref(s), p, p, ctypes.c_float(0.0), p, p, p, None) == la.LA_ERR_ARG
+    assert na(ctypes.byref(s), p, p, ctypes.c_float(float("nan")), p, p, p, None) == la.LA_ERR_ARG
+    assert na(ctypes.byref(s), None, p, ctypes.c_float(0.9), p, p, p, None) == la.LA_ERR_ARG
+    assert na(ctypes.byref(s), p, odd, ctypes.c_float(0.9), p, p, p, None) == la.LA_ERR_ARG
+    assert na(ctypes.byref(s), p, p, ctypes.c_float(0.9), p, p, None, None) == la.LA_ERR_ARG
+    assert na(None, p, p, ctypes.c_float(0.9), p, p, p, None) == la.LA_ERR_ARG
+    assert na(ctypes.byref(la.make_shape(1, 2, 256, 1024, 96, 64)), p, p, ctypes.c_float(0.9), p, p, p,
+              None) == la.LA_ERR_SHAPE
+    big = la.make_shape(1, 16, 6400, 6400 + 3000 * 64, 128, 64)      # 16 x 100 x (128 + 3000) x 4 B = 20 MB
+    assert na(ctypes.byref(big), p, p, ctypes.c_float(0.9), p, p, p, None) == la.LA_ERR_WORKSPACE
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     q = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16)
