@@ -7,13 +7,15 @@
 //     which chose the same context share a unit.  Its tiles are the 64-key sub-tiles of the
 //     union of its blocks' kept lists, in ascending key order, each tagged with which of the
 //     unit's blocks kept it.
-//   * A planner (two small kernels) computes the grouping, every unit's union list and
-//     one record per tile (first key, head, unit, ownership) in the concatenated tile sequence
-//     of all units.  One persistent workgroup per CU then takes an equal share of that sequence
-//     (stream-K); a unit cut between two workgroups leaves (O, m, l) partials that attn_combine
-//     merges with a log-sum-exp merge.  Heavy query blocks therefore never bound the launch.
-//   * Workgroup ranges are laid out so that the workgroups of one XCD hold consecutive units,
-//     i.e. the same heads: the shared chunk K/V of a head stays in that XCD's L2.
+//   * A planner (three small kernels) computes the grouping, every unit's union list, the
+//     schedule and one record per tile (first key, head, unit, ownership) in the tile sequence.
+//     One persistent workgroup per CU runs, first, whole units handed out in rounds: in each
+//     round the workgroups of one XCD start consecutive units of the same head together, so
+//     they walk that head's shared chunk K/V in step and each K/V tile reaches the XCD's L2
+//     about once per round; then an equal-work share of the remaining units (those past the
+//     last full round and the longer ones), cut anywhere (stream-K).  A unit cut between two
+//     shares leaves (O, m, l) partials that attn_combine merges with a log-sum-exp merge.  Heavy
+//     query blocks therefore never bound the launch.
 //
 // The workgroup: 8 waves = two groups of four, one wave of each group per SIMD.  Each wave owns
 // 32 query rows; the two waves of a SIMD own the two halves of the same query block, so both
@@ -467,35 +469,100 @@ __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t*
   if (tid == 0) ucount[u] = total;
 }
 
+// Where every unit's tiles go in the tile sequence, and which tiles each persistent workgroup
+// takes.  Units are handed out in two parts:
+//   * rounds of whole units: round r gives workgroup lambda = x PX + c (x its XCD, PX = P / 8
+//     workgroups per XCD) the unit x R PX + r PX + c, for r < R, unless that unit is longer than
+//     thr = T / (P R) tiles.  The workgroups of one XCD thus start consecutive units, i.e. query
+//     blocks of the same head, at the same time and walk the head's shared chunk K/V in step,
+//     so each K/V tile reaches that XCD's L2 about once per round instead of once per unit.  A
+//     workgroup's round units sit one after another at dp_start[lambda] .. dp_start[lambda + 1];
+//     by the length limit they add up to at most T / P tiles.
+//   * the other units (those past R P and the longer ones), concatenated in unit order after
+//     all round units, are shared by stream-K: workgroup lambda takes [sk_start[lambda],
+//     sk_start[lambda + 1]), sized so that its round tiles plus this share come as close as
+//     possible to T / P.  Units cut at these boundaries are merged afterwards.
+// R = (U - P / 4) / P leaves at least P / 4 units to the second part (when U >= P / 4), which
+// absorbs the differences in unit length.  tstart[u] = first tile of unit u; tstart[U] = T.
+// One workgroup of kPlanThreads >= P threads.
+__global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t* __restrict__ ucount, int U, int P,
+                                                                  int32_t* __restrict__ tstart,
+                                                                  int32_t* __restrict__ dp_start,
+                                                                  int32_t* __restrict__ sk_start) {
+  __shared__ int sh[kPlanThreads / 64];
+  const int tid = threadIdx.x;
+  const int PX = P >> 3;
+  const int R = U > P / 4 ? (U - P / 4) / P : 0;
+  const int U1 = R * P;                       // units considered for the rounds
+  auto tiles = [&](int u) { return max(1, ucount[u]); };
+  auto round_unit = [&](int lambda, int r) { return (lambda / PX) * R * PX + r * PX + lambda % PX; };
+  // each thread takes a contiguous run of units, so its loads are independent of each other
+  const int C = (U + kPlanThreads - 1) / kPlanThreads;
+  const int u_lo = min(U, tid * C), u_hi = min(U, u_lo + C);
+  int part = 0;
+  for (int u = u_lo; u < u_hi; ++u) part += tiles(u);
+  int T;
+  block_excl_scan_i(part, sh, &T);
+  const int thr = R > 0 ? max(1, (int)((int64_t)T / ((int64_t)P * R))) : 0;
+  auto in_rounds = [&](int u) { return u < U1 && tiles(u) <= thr; };
+  // round tiles of workgroup tid
+  int dp = 0;
+  if (tid < P)
+#pragma unroll 4
+    for (int r = 0; r < R; ++r) {
+      const int u = round_unit(tid, r);
+      if (in_rounds(u)) dp += tiles(u);
+    }
+  int Tdp;
+  const int dpa = block_excl_scan_i(dp, sh, &Tdp);
+  if (tid < P) {
+    dp_start[tid] = dpa;
+    int pos = dpa;
+    for (int r = 0; r < R; ++r) {
+      const int u = round_unit(tid, r);
+      if (in_rounds(u)) {
+        tstart[u] = pos;
+        pos += tiles(u);
+      }
+    }
+  }
+  if (tid == 0) dp_start[P] = Tdp;
+  // units of the second part, in unit order after the round units
+  int skp = 0;
+  for (int u = u_lo; u < u_hi; ++u)
+    if (!in_rounds(u)) skp += tiles(u);
+  int Tsk_sum;
+  int pos = Tdp + block_excl_scan_i(skp, sh, &Tsk_sum);
+  for (int u = u_lo; u < u_hi; ++u)
+    if (!in_rounds(u)) {
+      tstart[u] = pos;
+      pos += tiles(u);
+    }
+  const int Tsk = T - Tdp;
+  if (tid == 0) tstart[U] = T;
+  // second-part shares: quota q = max(0, ceil(T / P) - round tiles), scaled to the Tsk tiles
+  // (sum q >= P ceil(T / P) - Tdp >= Tsk, so no share exceeds its quota)
+  const int q = tid < P ? max(0, (T + P - 1) / P - dp) : 0;
+  int Q;
+  const int qa = block_excl_scan_i(q, sh, &Q);
+  if (tid < P) sk_start[tid] = Tdp + (Q > 0 ? (int)((int64_t)Tsk * qa / Q) : 0);
+  if (tid == 0) sk_start[P] = T;
+}
+
 // Expands unit u's union list into one record per 64-key tile at its place tstart[u] in the
-// global tile sequence, where tstart[u] = tiles of the units before u (summed here by the
-// workgroup); unit U-1 also writes tstart[U] = total.  With kvalid (valid keys at the front of
-// each key block), a tile's padding keys are counted into its flags.
+// tile sequence.  With kvalid (valid keys at the front of each key block), a tile's padding keys
+// are counted into its flags.
 __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t* __restrict__ ulist,
                                                                   const int32_t* __restrict__ ucount,
-                                                                  const int32_t* __restrict__ kvalid, int U, int NK,
-                                                                  int block, int row_tiles, int4* __restrict__ trec,
-                                                                  int32_t* __restrict__ tstart) {
-  __shared__ int sh[kPlanThreads / 64];
+                                                                  const int32_t* __restrict__ kvalid,
+                                                                  const int32_t* __restrict__ tstart, int NK,
+                                                                  int block, int row_tiles, int4* __restrict__ trec) {
   const int u = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63;
-  int part = 0;
-  for (int v = tid; v < u; v += kPlanThreads) part += max(1, ucount[v]);
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
-  if (lane == 0) sh[tid >> 6] = part;
-  __syncthreads();
-  int ts = 0;
-#pragma unroll
-  for (int wv = 0; wv < kPlanThreads / 64; ++wv) ts += sh[wv];
+  const int tid = threadIdx.x;
   const int nt = ucount[u], n = nt > 0 ? nt : 1;
   const int nsub = block / KT;
   const int bh = u / row_tiles;
-  if (tid == 0) {
-    tstart[u] = ts;
-    if (u == U - 1) tstart[U] = ts + n;
-  }
-  int4* out = trec + ts;
+  int4* out = trec + tstart[u];
   const int32_t* ul = ulist + (size_t)u * NK * nsub;
   for (int a = tid; a < n; a += kPlanThreads) {
     int key0 = 0, bits = 0;
@@ -513,43 +580,47 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t*
   }
 }
 
-// Stream lambda of P covers tiles [T lambda / P, T (lambda + 1) / P) of the global tile
-// sequence.
-__device__ inline int range_begin(int T, int lambda, int P) { return (int)((int64_t)T * lambda / P); }
+// The tiles of one workgroup: n1 round tiles from a1, then its stream-K share from a2; its tile
+// t (0 <= t < N) is tile at(t) of the sequence.
+struct WgTiles {
+  int a1, n1, a2, N;
+  __device__ int at(int t) const { return t < n1 ? a1 + t : a2 + (t - n1); }
+};
 
 // One tile of a workgroup's range (wave-uniform): record x = first key, y = (batch, head),
 // z = unit, w = ownership bits (0..3) | from0 | to_end (the unit's first / last tile), plus
-// first / last (the piece's, i.e. the unit's tiles inside this range) and valid.
+// first / last (the piece's, i.e. the unit's tiles inside this workgroup's round part or share)
+// and valid.
 struct TileRef {
   int key0, bh, unit, fl;
   __device__ bool valid() const { return fl & kFlValid; }
   __device__ bool owned(int list) const { return (fl >> list) & 1; }
 };
 
-__device__ inline TileRef make_tile(const int4& e, int t, int t_begin, int t_end) {
+__device__ inline TileRef make_tile(const int4& e, int t, const WgTiles& g) {
   TileRef r{0, 0, 0, 0};
-  if (t < t_end) {
+  if (t < g.N) {
     r.key0 = e.x;
     r.bh = e.y;
     r.unit = e.z;
-    r.fl = e.w | kFlValid | ((e.w & kFlFrom0) || t == t_begin ? kFlFirst : 0) |
-           ((e.w & kFlToEnd) || t + 1 == t_end ? kFlLast : 0);
+    r.fl = e.w | kFlValid | ((e.w & kFlFrom0) || t == 0 || t == g.n1 ? kFlFirst : 0) |
+           ((e.w & kFlToEnd) || t + 1 == g.N ? kFlLast : 0);
   }
   return r;
 }
 
-// The record of tile t, read through the constant address space: the records are written by
-// an earlier kernel and never during this one, so the loads can go through the scalar cache
-// (s_load).  Index t is clamped into the range (t_end > t_begin); make_tile ignores a record
-// past the end.
+// The record of the workgroup's tile t, read through the constant address space: the records
+// are written by an earlier kernel and never during this one, so the loads can go through the
+// scalar cache (s_load).  t is clamped to the last tile (N > 0); make_tile ignores a record past
+// the end.
 typedef __attribute__((address_space(4))) const int cint32;
-__device__ inline int4 load_tile(const int4* __restrict__ trec, int t, int t_end) {
-  const cint32* r = (const cint32*)(trec + (t < t_end ? t : t_end - 1));
+__device__ inline int4 load_tile(const int4* __restrict__ trec, int t, const WgTiles& g) {
+  const cint32* r = (const cint32*)(trec + g.at(t < g.N ? t : g.N - 1));
   return int4{r[0], r[1], r[2], r[3]};
 }
 
-__device__ inline TileRef fetch_tile(const int4* __restrict__ trec, int t, int t_begin, int t_end) {
-  return make_tile(load_tile(trec, t, t_end), t, t_begin, t_end);
+__device__ inline TileRef fetch_tile(const int4* __restrict__ trec, int t, const WgTiles& g) {
+  return make_tile(load_tile(trec, t, g), t, g);
 }
 
 // State of one wave's running unit piece.
@@ -687,23 +758,26 @@ __device__ __forceinline__ void v_phase(WaveState<D>& st, const WaveCtx& w, cons
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    const int4* __restrict__ trec, const int32_t* __restrict__ tstart, const int32_t* __restrict__ qmap,
-    uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ part_o, float* __restrict__ part_m,
-    float* __restrict__ part_l, Geom gm, int U, float scale_log2) {
+    const int4* __restrict__ trec, const int32_t* __restrict__ dp_start, const int32_t* __restrict__ sk_start,
+    const int32_t* __restrict__ qmap, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ part_o,
+    float* __restrict__ part_m, float* __restrict__ part_l, Geom gm, float scale_log2) {
   using T = Tile<D>;
   __shared__ __attribute__((aligned(1024))) unsigned char kb0[T::KBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char kb1[T::KBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char vb0[T::VBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char vb1[T::VBYTES];
 
-  // XCD-aware range: hardware places consecutive workgroup ids on consecutive XCDs (round
-  // robin over 8); the workgroups of one XCD get consecutive ranges, i.e. consecutive units
-  // of the same heads, so each L2 keeps its heads' shared K/V.  P is a multiple of 8.
+  // XCD-aware numbering: hardware places consecutive workgroup ids on consecutive XCDs (round
+  // robin over 8); lambda = x PX + c numbers the workgroups of XCD x consecutively, which is
+  // the numbering the plan hands out its units in.  P is a multiple of 8.
   const int P = gridDim.x;
   const int lambda = (blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3);
-  const int Ttot = tstart[U];
-  const int t_begin = range_begin(Ttot, lambda, P), t_end = range_begin(Ttot, lambda + 1, P);
-  if (t_begin >= t_end) return;
+  WgTiles g;
+  g.a1 = dp_start[lambda];
+  g.n1 = dp_start[lambda + 1] - g.a1;
+  g.a2 = sk_start[lambda];
+  g.N = g.n1 + sk_start[lambda + 1] - g.a2;
+  if (g.N <= 0) return;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps tile-issue math scalar
@@ -762,10 +836,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   st.r0w = 0;
   st.bh = 0;
 
-  const int N = t_end - t_begin;
+  const int N = g.N;
   int prev_fl = 0, prev_key0 = 0;      // the previous tile: flags and first key
-  TileRef cur = fetch_tile(trec, t_begin, t_begin, t_end);
-  TileRef nxt = fetch_tile(trec, t_begin + 1, t_begin, t_end);
+  TileRef cur = fetch_tile(trec, 0, g);
+  TileRef nxt = fetch_tile(trec, 1, g);
 
   // this (group 1) wave's loads of K(tile tk) into kdst and V(tile tv) into vdst
   auto issue_loads = [&](unsigned char* kdst, const TileRef& tk, unsigned char* vdst, const TileRef& tv) {
@@ -800,14 +874,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       if constexpr (!IS_G1) {
         m_phase<D>(st, w, prev_fl, cur, kc, vp, ka);
         lds_barrier();
-        const int4 raw = load_tile(trec, t_begin + hh + 2, t_end);
+        const int4 raw = load_tile(trec, hh + 2, g);
         v_phase<D>(st, w, cur, ka);
-        nx2 = make_tile(raw, t_begin + hh + 2, t_begin, t_end);
+        nx2 = make_tile(raw, hh + 2, g);
         lds_barrier();
       } else {
-        const int4 raw = load_tile(trec, t_begin + hh + 2, t_end);
+        const int4 raw = load_tile(trec, hh + 2, g);
         v_phase<D>(st, w, TileRef{prev_key0, 0, 0, prev_fl}, ka);
-        nx2 = make_tile(raw, t_begin + hh + 2, t_begin, t_end);
+        nx2 = make_tile(raw, hh + 2, g);
         issue_loads(kn, nxt, vc, cur);
         barrier_keep_loads();
         m_phase<D>(st, w, prev_fl, cur, kc, vp, ka);
@@ -834,17 +908,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   else run(std::false_type{});
 }
 
-// Merges the pieces of units that were split across streams:
-// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s, over the pieces in stream order
+// Merges the pieces of units that were split across the stream-K shares of the workgroups:
+// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s, over the pieces in share order
 // (deterministic).  Workgroup (lambda, c) handles rows [32 c, 32 c + 32) of the unit that starts
-// inside stream lambda's range and continues past it, if there is one (each split unit has
-// exactly one such stream).
+// inside workgroup lambda's share and continues past it, if there is one (each split unit has
+// exactly one such share).  Units handed out in rounds are never split.
 constexpr int kCombRows = 32;
 constexpr int kCombThreads = 256;
 
 template <int D>
 __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_t* __restrict__ tstart,
-                                                                    const int32_t* __restrict__ qmap, int U, int P,
+                                                                    const int32_t* __restrict__ ucount,
+                                                                    const int32_t* __restrict__ sk_start,
+                                                                    const int4* __restrict__ trec,
+                                                                    const int32_t* __restrict__ qmap, int P,
                                                                     int row_tiles, int Lq, int block,
                                                                     const float* __restrict__ part_o,
                                                                     const float* __restrict__ part_m,
@@ -855,24 +932,27 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
   constexpr int RSTEP = kCombThreads / CG;     // rows per pass
   constexpr int NI = kCombRows / RSTEP;        // rows per thread
   const int lam0 = blockIdx.x;
-  const int Ttot = tstart[U];
-  const int b = range_begin(Ttot, lam0, P), e = range_begin(Ttot, lam0 + 1, P);
+  const int b = sk_start[lam0], e = sk_start[lam0 + 1];
   if (b >= e) return;
-  // unit holding tile e - 1: largest u with tstart[u] <= e - 1
-  int lo = 0, hi = U - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (tstart[mid] <= e - 1) lo = mid;
-    else hi = mid - 1;
-  }
-  const int u = lo;
-  const int ts = tstart[u], te = tstart[u + 1];
+  // unit holding tile e - 1: its record names it
+  const int u = trec[e - 1].z;
+  const int ts = tstart[u], te = ts + max(1, ucount[u]);
   if (ts < b || te <= e) return;
-  // stream holding tile t: largest lambda with T lambda / P <= t
-  auto owner = [&](int t) {
-    const int64_t lam = ((int64_t)(t + 1) * P + Ttot - 1) / Ttot - 1;
-    return (int)(lam < P - 1 ? lam : P - 1);
-  };
+  // The pieces of the unit, in share order: the last piece of this share (slot 2 lam0 + 1), then
+  // the first piece (slot 2 lambda) of every later non-empty share that starts before the unit
+  // ends.  Their slots are listed in LDS first, so that the loads of several pieces can be in
+  // flight together.
+  __shared__ int sh[kCombThreads / 64];
+  __shared__ int pslot[kMaxPersist + 1];
+  const int lam = lam0 + 1 + threadIdx.x;
+  const int a = lam < P ? sk_start[lam] : 0, z = lam < P ? sk_start[lam + 1] : 0;
+  const int take = lam < P && a < z && a < te;
+  int np;
+  const int pos = block_excl_scan_i(take, sh, &np);
+  if (take) pslot[1 + pos] = 2 * lam;
+  if (threadIdx.x == 0) pslot[0] = 2 * lam0 + 1;
+  __syncthreads();
+  np += 1;
   const int bh = u / row_tiles;
   const int cg = threadIdx.x % CG, r0 = blockIdx.y * kCombRows + threadIdx.x / CG;
   float m[NI], l[NI];
@@ -883,29 +963,26 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
     l[i] = 0.f;
     acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // The pieces of the unit, in stream order: the last piece of this range (slot 2 lam0 + 1),
-  // then one piece in each later non-empty range up to the one holding tile te - 1 (slot 2 lam:
-  // the first piece of that range).  Streams are visited through the tiles they hold, so empty
-  // ranges (fewer tiles than streams) cost nothing.
-  for (int pass = 0; pass < 2; ++pass) {
-    int lam = lam0, next = e;
-    while (true) {
-      const int slot = lam == lam0 ? 2 * lam + 1 : 2 * lam;
+  // two passes without branches, so that the loads of many pieces are in flight together: the
+  // row max over the pieces, then the pieces weighted by 2^(m_s - m) (0 for an empty piece)
+#pragma unroll 8
+  for (int pc = 0; pc < np; ++pc) {
+    const size_t pr0 = (size_t)pslot[pc] * QR + r0;
 #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const size_t pr = (size_t)slot * QR + r0 + RSTEP * i;
-        if (pass == 0) {
-          m[i] = fmaxf(m[i], part_m[pr]);
-        } else {
-          const float wgt = exp2f(part_m[pr] - (m[i] == -INFINITY ? 0.f : m[i]));
-          l[i] += wgt * part_l[pr];
-          const f32x4 po = *(const f32x4*)(part_o + pr * D + 4 * cg);
-          acc[i] += wgt * po;
-        }
-      }
-      if (next >= te) break;
-      lam = owner(next);
-      next = range_begin(Ttot, lam + 1, P);
+    for (int i = 0; i < NI; ++i) m[i] = fmaxf(m[i], part_m[pr0 + RSTEP * i]);
+  }
+  float mu[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) mu[i] = m[i] == -INFINITY ? 0.f : m[i];
+#pragma unroll 4
+  for (int pc = 0; pc < np; ++pc) {
+    const size_t pr0 = (size_t)pslot[pc] * QR + r0;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const size_t pr = pr0 + RSTEP * i;
+      const float wgt = exp2f(part_m[pr] - mu[i]);
+      l[i] += wgt * part_l[pr];
+      acc[i] += wgt * *(const f32x4*)(part_o + pr * D + 4 * cg);
     }
   }
 #pragma unroll
@@ -931,6 +1008,8 @@ struct AttnWs {
   int32_t* ulist;
   int32_t* ucount;
   int32_t* tstart;
+  int32_t* dp_start;
+  int32_t* sk_start;
   float* part_o;
   float* part_m;
   float* part_l;
@@ -955,6 +1034,10 @@ AttnWs attn_ws_layout(const Dims& dm, void* base) {
   off += align256(U * sizeof(int32_t));
   w.tstart = (int32_t*)(b + off);
   off += align256((U + 1) * sizeof(int32_t));
+  w.dp_start = (int32_t*)(b + off);
+  off += align256((kMaxPersist + 1) * sizeof(int32_t));
+  w.sk_start = (int32_t*)(b + off);
+  off += align256((kMaxPersist + 1) * sizeof(int32_t));
   w.part_o = (float*)(b + off);
   off += align256(slots * QR * dm.d * sizeof(float));
   w.part_m = (float*)(b + off);
@@ -988,42 +1071,41 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
                      st, counts, idx, kvalid, dm.NQ, dm.NK, dm.h0, dm.h1, dm.Lk, dm.block, row_tiles, w.qmap,
                      w.ulist, w.ucount);
-  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U, dm.NK,
-                     dm.block, row_tiles, w.trec, w.tstart);
+  hipLaunchKernelGGL(plan_sched_kernel, dim3(1), dim3(kPlanThreads), 0, st, w.ucount, U, persistent_workgroups(),
+                     w.tstart, w.dp_start, w.sk_start);
+  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, w.tstart,
+                     dm.NK, dm.block, row_tiles, w.trec);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_run(const Dims& dm, const void* q, const void* k, const void* v, float scale, void* o,
                            float* lse, void* ws, hipStream_t st) {
-  const int row_tiles = ceil_div(dm.Lq, QR);
-  const int U = dm.BH * row_tiles;
   const int P = persistent_workgroups();
   AttnWs w = attn_ws_layout(dm, ws);
   Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
   const float scale_log2 = scale * 1.4426950408889634f;
   if (dm.d == 128)
     hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, w.qmap, (uint16_t*)o, lse,
-                       w.part_o, w.part_m, w.part_l, gm, U, scale_log2);
+                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.dp_start, w.sk_start, w.qmap,
+                       (uint16_t*)o, lse, w.part_o, w.part_m, w.part_l, gm, scale_log2);
   else
     hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.tstart, w.qmap, (uint16_t*)o, lse,
-                       w.part_o, w.part_m, w.part_l, gm, U, scale_log2);
+                       (const uint16_t*)k, (const uint16_t*)v, w.trec, w.dp_start, w.sk_start, w.qmap,
+                       (uint16_t*)o, lse, w.part_o, w.part_m, w.part_l, gm, scale_log2);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipStream_t st) {
   const int row_tiles = ceil_div(dm.Lq, QR);
-  const int U = dm.BH * row_tiles;
   const int P = persistent_workgroups();
   AttnWs w = attn_ws_layout(dm, ws);
   const dim3 cgrid(P, QR / kCombRows);
   if (dm.d == 128)
-    hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.qmap, U, P, row_tiles,
-                       dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
+    hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.ucount, w.sk_start, w.trec,
+                       w.qmap, P, row_tiles, dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<64>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.qmap, U, P, row_tiles,
-                       dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
+    hipLaunchKernelGGL(attn_combine_kernel<64>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.ucount, w.sk_start, w.trec,
+                       w.qmap, P, row_tiles, dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   return hipGetLastError();
 }
 
