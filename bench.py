@@ -11,6 +11,10 @@ entry point so that HIP events on the launch stream time every stage.  Prints ON
 NAME may also be a 3-D block workload (480p_3d, 720p_3d, tiny_3d): then a step is the 3-D path
 (Q-Prep, KV-Prep, selection from the pooled means, attention, Untile Scatter).
 
+Before the W warm-up steps the step is repeated for --clock-warmup-ms of wall time (200 ms by
+default, reported as clock_warmup): the GPU's clock ramps up over the first milliseconds of work,
+and without this the timed steps of the short workloads would partly run before it has.
+
 value = kept-block TFLOP/s of the whole step (kept FLOPs / step time).  The line also
 carries the per-kernel split, the dense baseline (same attention kernel, every block
 kept), the roofline of the attention kernel (la_sparse_attn_run launches exactly that one
@@ -51,6 +55,9 @@ def parse():
                     help="also time the attention run with the caches flushed (512 MiB written between calls)")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps of the sparse path only (for rocprofv3), print the JSON anyway")
+    ap.add_argument("--clock-warmup-ms", type=float, default=200.0,
+                    help="before the warm-up steps, repeat the step for this much wall time so that the timed "
+                         "steps run at the GPU's steady clock (0: off; off with --profile-only)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device-to-device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -84,6 +91,23 @@ def traffic_from_profile(kernel_tag: str, workload: str, digest: str, launches_b
     if rec.get("src_digest") != digest:
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def clock_warmup(stages, ms: float):
+    """Repeats the step (the bound calls in order) until `ms` of wall time have passed; returns
+    (steps, elapsed ms).  The first milliseconds of GPU work in a process run up to ~13 % slower
+    (the clock ramps up), which would otherwise bias the short workloads' timed steps."""
+    import torch
+    if ms <= 0:
+        return 0, 0.0
+    n, t0 = 0, time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(8):
+            for f in stages:
+                f()
+        n += 8
+        torch.cuda.synchronize()
+    return n, round((time.perf_counter() - t0) * 1e3, 1)
 
 
 def kept_flop_count(mask_np, Lq: int, Lk: int, block: int, d: int) -> int:
@@ -264,6 +288,7 @@ def main_3d(args, wl):
     names = ("prep_q", "prep_kv", "select", "attn_plan", "attn_run", "attn_merge", "untile")
     if args.calibrate_copy:
         calibration_copy(dev)
+    cw = clock_warmup(stages, 0.0 if args.profile_only else args.clock_warmup_ms)
     for _ in range(args.warmup):
         for f in stages:
             f()
@@ -327,6 +352,7 @@ def main_3d(args, wl):
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
+        "clock_warmup": {"steps": cw[0], "ms": cw[1]},
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -412,6 +438,7 @@ def main():
 
     if args.calibrate_copy:
         calibration_copy(dev)
+    cw = clock_warmup(stages, 0.0 if args.profile_only else args.clock_warmup_ms)
     for _ in range(args.warmup):
         for f in stages:
             f()
@@ -513,6 +540,7 @@ def main():
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
+        "clock_warmup": {"steps": cw[0], "ms": cw[1]},
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
