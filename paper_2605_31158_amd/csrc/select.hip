@@ -4,9 +4,9 @@
 //   pool_q        one wave per (head, query block): mean of the block's valid rows
 //                 -> q_bar fp32 [BH, NQ, d] (workspace).  Streaming read, every load of a
 //                 lane in flight at once.
-//   pool_k_score  one workgroup per (head, group of GB historical key blocks): each wave pools
+//   pool_k_score  one workgroup per (head, group of G <= 32 historical key blocks): each wave pools
 //                 whole blocks into LDS (never written out), then the workgroup scores the
-//                 GB pooled keys against every pooled query of the head with fp32 MFMA
+//                 G pooled keys against every pooled query of the head with fp32 MFMA
 //                 (v_mfma_f32_16x16x4_f32) -> s fp32 [BH, NQ, M] (workspace).  The K read is
 //                 the dominant cost of selection; it is one coalesced streaming pass.
 //   select_rows   one wave per (head, query block), no workgroup barriers: softmax over the
@@ -108,19 +108,20 @@ template <int D, int BLOCK, int GB, bool POOLED>
 __global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const void* __restrict__ kin,
                                                                 const float* __restrict__ qbar,
                                                                 float* __restrict__ scores, int Lk, int NK, int NQ,
-                                                                int h0, int M, float inv_sqrt_d) {
+                                                                int h0, int M, int G, float inv_sqrt_d) {
   constexpr int LD = D + kPadF;
   __shared__ __attribute__((aligned(16))) float kb[GB][LD];
   __shared__ __attribute__((aligned(16))) float qb[kQChunk][LD];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = blockIdx.y;
-  const int m0 = blockIdx.x * GB;
-  const int gcount = min(GB, M - m0);
+  const int m0 = blockIdx.x * G;               // G <= GB key blocks per workgroup
+  const int gcount = min(G, M - m0);
+  const int gpad = (gcount + 15) & ~15;          // rows of kb the MFMA tiles read
   constexpr int CH = D / 8;
   const float inv_block = 1.0f / (float)BLOCK;
   const uint16_t* __restrict__ k = (const uint16_t*)kin;
   const float* __restrict__ kbar = (const float*)kin;
-  for (int g = wave; g < GB; g += kScoreThreads / 64) {
+  for (int g = wave; g < gpad; g += kScoreThreads / 64) {
     if (POOLED) {
       if (lane < D / 4) {
         f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -142,8 +143,8 @@ __global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const void*
   }
   // S tile [query rows x GB] = q_bar (rows x D) . k_bar^T (D x GB), 16x16 MFMA tiles:
   // lane l supplies A[row l%16][k l/16] and B[k l/16][col l%16]; C rows 4(l/16)+i, col l%16.
-  constexpr int CT = GB / 16;                     // column tiles
-  constexpr int NT = (kQChunk / 16) * CT;         // tiles per query chunk
+  const int CT = gpad / 16;                       // column tiles
+  const int NT = (kQChunk / 16) * CT;             // tiles per query chunk
   const int c16 = lane & 15, k4 = lane >> 4;
   for (int i0 = 0; i0 < NQ; i0 += kQChunk) {
     __syncthreads();                              // kb complete / previous chunk consumed
@@ -444,16 +445,31 @@ __global__ __launch_bounds__(kThreads) void mask_to_list_kernel(const uint8_t* _
 }
 
 // Scores of the pooled keys (pooled here from k, or given as kbar when POOLED) against qbar.
+// Key blocks per workgroup when the keys are pooled here: the grid should fill the resident
+// workgroup slots of the device
+// (about three per CU, LDS-bound) in as few, as full rounds as possible: G = blocks / (rounds x
+// slots), at most 32 (the LDS tile) and at least 8 (each workgroup stages the head's pooled
+// queries once), so that no round runs on a fraction of the CUs.
+inline int score_group(const Dims& dm) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    cus = 256;
+  const int64_t slots = 3 * (int64_t)cus;
+  const int64_t blocks = (int64_t)dm.BH * dm.M;
+  const int64_t rounds = (blocks + 32 * slots - 1) / (32 * slots);
+  const int64_t g = (blocks + rounds * slots - 1) / (rounds * slots);
+  return (int)(g < 8 ? 8 : g > 32 ? 32 : g);
+}
+
 template <int D, int BLOCK, bool POOLED>
 void launch_score(const Dims& dm, const void* kin, const float* qbar, float* scores, hipStream_t st) {
   const float inv_sqrt_d = 1.0f / sqrtf((float)dm.d);
-  // 32 key blocks per workgroup when that still gives >= 1 workgroup per CU, else 16
-  if ((int64_t)ceil_div(dm.M, 32) * dm.BH >= 256)
-    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 32, POOLED>), dim3(ceil_div(dm.M, 32), dm.BH),
-                       dim3(kScoreThreads), 0, st, kin, qbar, scores, dm.Lk, dm.NK, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
-  else
-    hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 16, POOLED>), dim3(ceil_div(dm.M, 16), dm.BH),
-                       dim3(kScoreThreads), 0, st, kin, qbar, scores, dm.Lk, dm.NK, dm.NQ, dm.h0, dm.M, inv_sqrt_d);
+  // pooled means in: the work is the scoring, so fewer, fuller workgroups (32 blocks when that
+  // still gives one per CU, else 16)
+  const int G = POOLED ? ((int64_t)ceil_div(dm.M, 32) * dm.BH >= 256 ? 32 : 16) : score_group(dm);
+  hipLaunchKernelGGL((pool_k_score_kernel<D, BLOCK, 32, POOLED>), dim3(ceil_div(dm.M, G), dm.BH),
+                     dim3(kScoreThreads), 0, st, kin, qbar, scores, dm.Lk, dm.NK, dm.NQ, dm.h0, dm.M, G, inv_sqrt_d);
 }
 
 template <int D, int BLOCK>
