@@ -931,6 +931,7 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
   constexpr int CG = D / 4;                    // 4-column groups per row
   constexpr int RSTEP = kCombThreads / CG;     // rows per pass
   constexpr int NI = kCombRows / RSTEP;        // rows per thread
+  constexpr int BATCH = 4;                     // pieces whose loads are in flight together
   const int lam0 = blockIdx.x;
   const int b = sk_start[lam0], e = sk_start[lam0 + 1];
   if (b >= e) return;
@@ -963,26 +964,40 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
     l[i] = 0.f;
     acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // two passes without branches, so that the loads of many pieces are in flight together: the
-  // row max over the pieces, then the pieces weighted by 2^(m_s - m) (0 for an empty piece)
-#pragma unroll 8
-  for (int pc = 0; pc < np; ++pc) {
-    const size_t pr0 = (size_t)pslot[pc] * QR + r0;
+  // batches of pieces: all loads of a batch first, then one rescale of the running (m, l, O) to
+  // the batch's max and the pieces added with weights 2^(m_s - m) (0 for an empty piece or a
+  // slot past the last piece); no branches, so the loads of a batch overlap
+  for (int pc0 = 0; pc0 < np; pc0 += BATCH) {
+    float bm[BATCH][NI], bl[BATCH][NI];
+    f32x4 bo[BATCH][NI];
 #pragma unroll
-    for (int i = 0; i < NI; ++i) m[i] = fmaxf(m[i], part_m[pr0 + RSTEP * i]);
-  }
-  float mu[NI];
+    for (int j = 0; j < BATCH; ++j) {
+      const bool ok = pc0 + j < np;
+      const size_t pr0 = (size_t)pslot[ok ? pc0 + j : 0] * QR + r0;
 #pragma unroll
-  for (int i = 0; i < NI; ++i) mu[i] = m[i] == -INFINITY ? 0.f : m[i];
-#pragma unroll 4
-  for (int pc = 0; pc < np; ++pc) {
-    const size_t pr0 = (size_t)pslot[pc] * QR + r0;
+      for (int i = 0; i < NI; ++i) {
+        const size_t pr = pr0 + RSTEP * i;
+        bm[j][i] = ok ? part_m[pr] : -INFINITY;
+        bl[j][i] = ok ? part_l[pr] : 0.f;
+        bo[j][i] = ok ? *(const f32x4*)(part_o + pr * D + 4 * cg) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const size_t pr = pr0 + RSTEP * i;
-      const float wgt = exp2f(part_m[pr] - mu[i]);
-      l[i] += wgt * part_l[pr];
-      acc[i] += wgt * *(const f32x4*)(part_o + pr * D + 4 * cg);
+      float mn = m[i];
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) mn = fmaxf(mn, bm[j][i]);
+      const float mu = mn == -INFINITY ? 0.f : mn;
+      const float a = exp2f(m[i] - mu);                // 0 while the running max is -inf
+      l[i] *= a;
+      acc[i] *= a;
+#pragma unroll
+      for (int j = 0; j < BATCH; ++j) {
+        const float wgt = exp2f(bm[j][i] - mu);
+        l[i] += wgt * bl[j][i];
+        acc[i] += wgt * bo[j][i];
+      }
+      m[i] = mn;
     }
   }
 #pragma unroll
