@@ -144,8 +144,10 @@ la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k
  * head grouped by the first historical entry of their lists, the first kept historical
  * block for the ascending lists the selection writes; any order gives the same results),
  * the union of their lists as
- * 64-key tiles, and the split of all tiles into equal ranges over one persistent
- * workgroup per CU.  It lives in ws.
+ * 64-key tiles, and the split of the work over one persistent workgroup per CU of the
+ * current device: whole units in rounds (the workgroups of one XCD start consecutive
+ * units of a head together), the remaining and the longest units in equal-work shares
+ * cut anywhere.  It lives in ws and is for the device it was built on.
  *
  * la_sparse_attn_plan: builds the plan for `shape` from counts/idx (read as in
  *   la_sparse_attn_fwd) into ws.

@@ -542,7 +542,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t*
   if (tid == 0) tstart[U] = T;
   // second-part shares: quota q = max(0, ceil(T / P) - round tiles), scaled to the Tsk tiles
   // (sum q >= P ceil(T / P) - Tdp >= Tsk, so no share exceeds its quota)
-  const int q = tid < P ? max(0, (T + P - 1) / P - dp) : 0;
+  const int q = tid < P ? max(0, (int)(((int64_t)T + P - 1) / P) - dp) : 0;
   int Q;
   const int qa = block_excl_scan_i(q, sh, &Q);
   if (tid < P) sk_start[tid] = Tdp + (Q > 0 ? (int)((int64_t)Tsk * qa / Q) : 0);
