@@ -587,7 +587,7 @@ struct WgTiles {
   __device__ int at(int t) const { return t < n1 ? a1 + t : a2 + (t - n1); }
 };
 
-// One tile of a workgroup's range (wave-uniform): record x = first key, y = (batch, head),
+// One tile of a workgroup's work (wave-uniform): record x = first key, y = (batch, head),
 // z = unit, w = ownership bits (0..3) | from0 | to_end (the unit's first / last tile), plus
 // first / last (the piece's, i.e. the unit's tiles inside this workgroup's round part or share)
 // and valid.
@@ -692,8 +692,9 @@ __device__ __forceinline__ void start_piece(WaveState<D>& st, WaveCtx& w, const 
 }
 
 // Ends a piece: the normalised bf16 output (and lse) when the piece is the whole unit, else the
-// fp32 partial (O unnormalised, running max m, sum l) in slot 2 lambda (the range's first piece,
-// which continues an earlier range) or 2 lambda + 1 (its last, continued by a later range).
+// fp32 partial (O unnormalised, running max m, sum l) in slot 2 lambda (the first piece of the
+// workgroup's stream-K share, which continues an earlier share) or 2 lambda + 1 (its last,
+// continued by a later share).
 // The stores are completed before returning (the tile-load waits count only tile loads).
 template <int D>
 __device__ __forceinline__ void end_piece(const WaveState<D>& st, bool to_end, const KArgs& ka) {
