@@ -181,6 +181,7 @@ struct LoadSet {
 
 struct Geom {
   int Lq, Lk, block, NQ, NK, F, chunk0;
+  int BH, U;          // heads and units of the plan (bounds for the fields read from it)
 };
 
 // Per-wave constants of the tile loop (klimit, klimit_wave change with the unit).
@@ -584,6 +585,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t*
 // t (0 <= t < N) is tile at(t) of the sequence.
 struct WgTiles {
   int a1, n1, a2, N;
+  int Lk, BH, U;          // bounds of a record's first key, head and unit
   __device__ int at(int t) const { return t < n1 ? a1 + t : a2 + (t - n1); }
 };
 
@@ -600,9 +602,11 @@ struct TileRef {
 __device__ inline TileRef make_tile(const int4& e, int t, const WgTiles& g) {
   TileRef r{0, 0, 0, 0};
   if (t < g.N) {
-    r.key0 = e.x;
-    r.bh = e.y;
-    r.unit = e.z;
+    // the fields are clamped into range, so that even a plan the workspace no longer holds
+    // (overwritten by another call) reads and writes inside q, k, v, o and the workspace
+    r.key0 = min(max(e.x, 0), g.Lk);
+    r.bh = min(max(e.y, 0), g.BH - 1);
+    r.unit = min(max(e.z, 0), g.U - 1);
     r.fl = e.w | kFlValid | ((e.w & kFlFrom0) || t == 0 || t == g.n1 ? kFlFirst : 0) |
            ((e.w & kFlToEnd) || t + 1 == g.N ? kFlLast : 0);
   }
@@ -662,7 +666,7 @@ __device__ __forceinline__ void start_piece(WaveState<D>& st, WaveCtx& w, const 
   const Geom& gm = ka.gm;
   st.bh = t.bh;
   const int qb = ka.qmap[(size_t)t.unit * (QR / gm.block) + ka.my_list];
-  st.r0w = qb >= 0 ? qb * gm.block + ka.r_sub : gm.Lq;
+  st.r0w = qb >= 0 && qb < gm.NQ ? qb * gm.block + ka.r_sub : gm.Lq;
   st.rows = st.r0w < gm.Lq;
   st.from0 = t.fl & kFlFrom0;
   st.m_run = -INFINITY;
@@ -761,7 +765,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const int4* __restrict__ trec, const int32_t* __restrict__ dp_start, const int32_t* __restrict__ sk_start,
     const int32_t* __restrict__ qmap, uint16_t* __restrict__ o, float* __restrict__ lse, float* __restrict__ part_o,
-    float* __restrict__ part_m, float* __restrict__ part_l, Geom gm, float scale_log2) {
+    float* __restrict__ part_m, float* __restrict__ part_l, Geom gm, int Tcap, float scale_log2) {
   using T = Tile<D>;
   __shared__ __attribute__((aligned(1024))) unsigned char kb0[T::KBYTES];
   __shared__ __attribute__((aligned(1024))) unsigned char kb1[T::KBYTES];
@@ -773,11 +777,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // the numbering the plan hands out its units in.  P is a multiple of 8.
   const int P = gridDim.x;
   const int lambda = (blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3);
+  // the workgroup's tiles, clamped into the record array (Tcap records)
   WgTiles g;
-  g.a1 = dp_start[lambda];
-  g.n1 = dp_start[lambda + 1] - g.a1;
-  g.a2 = sk_start[lambda];
-  g.N = g.n1 + sk_start[lambda + 1] - g.a2;
+  g.a1 = min(max(dp_start[lambda], 0), Tcap);
+  g.n1 = min(max(dp_start[lambda + 1] - g.a1, 0), Tcap - g.a1);
+  g.a2 = min(max(sk_start[lambda], 0), Tcap);
+  g.N = g.n1 + min(max(sk_start[lambda + 1] - g.a2, 0), Tcap - g.a2);
+  g.Lk = gm.Lk;
+  g.BH = gm.BH;
+  g.U = gm.U;
   if (g.N <= 0) return;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -922,8 +930,8 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
                                                                     const int32_t* __restrict__ ucount,
                                                                     const int32_t* __restrict__ sk_start,
                                                                     const int4* __restrict__ trec,
-                                                                    const int32_t* __restrict__ qmap, int P,
-                                                                    int row_tiles, int Lq, int block,
+                                                                    const int32_t* __restrict__ qmap, int P, int U,
+                                                                    int Tcap, int row_tiles, int Lq, int block,
                                                                     const float* __restrict__ part_o,
                                                                     const float* __restrict__ part_m,
                                                                     const float* __restrict__ part_l,
@@ -934,10 +942,10 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
   constexpr int NI = kCombRows / RSTEP;        // rows per thread
   constexpr int BATCH = 4;                     // pieces whose loads are in flight together
   const int lam0 = blockIdx.x;
-  const int b = sk_start[lam0], e = sk_start[lam0 + 1];
+  const int b = min(max(sk_start[lam0], 0), Tcap), e = min(max(sk_start[lam0 + 1], 0), Tcap);
   if (b >= e) return;
-  // unit holding tile e - 1: its record names it
-  const int u = trec[e - 1].z;
+  // unit holding tile e - 1: its record names it (clamped, like every index read from the plan)
+  const int u = min(max(trec[e - 1].z, 0), U - 1);
   const int ts = tstart[u], te = ts + max(1, ucount[u]);
   if (ts < b || te <= e) return;
   // The pieces of the unit, in share order: the last piece of this share (slot 2 lam0 + 1), then
@@ -1006,7 +1014,7 @@ __global__ __launch_bounds__(kCombThreads) void attn_combine_kernel(const int32_
     const int r = r0 + RSTEP * i;                       // row inside the unit
     const int qb = qmap[(size_t)u * (QR / block) + r / block];
     const int qrow = qb * block + r % block;
-    if (qb >= 0 && qrow < Lq) {
+    if (qb >= 0 && qb <= Lq / block && qrow < Lq) {
       const float inv = l[i] > 0.f ? 1.0f / l[i] : 0.f;
       u32x2 ow;
       ow[0] = pack_bf16x2(acc[i][0] * inv, acc[i][1] * inv);
@@ -1031,6 +1039,11 @@ struct AttnWs {
   float* part_l;
   size_t bytes;
 };
+
+// Records the workspace holds: at most max(1, NK (block / 64)) tiles per unit.
+size_t attn_tile_capacity(const Dims& dm) {
+  return (size_t)dm.BH * ceil_div(dm.Lq, QR) * (size_t)dm.NK * (dm.block / KT);
+}
 
 AttnWs attn_ws_layout(const Dims& dm, void* base) {
   const int row_tiles = ceil_div(dm.Lq, QR);
@@ -1098,16 +1111,17 @@ hipError_t launch_attn_run(const Dims& dm, const void* q, const void* k, const v
                            float* lse, void* ws, hipStream_t st) {
   const int P = persistent_workgroups();
   AttnWs w = attn_ws_layout(dm, ws);
-  Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0};
+  const int Tcap = (int)attn_tile_capacity(dm);
+  Geom gm{dm.Lq, dm.Lk, dm.block, dm.NQ, dm.NK, dm.frame_tokens, dm.chunk0, dm.BH, dm.BH * ceil_div(dm.Lq, QR)};
   const float scale_log2 = scale * 1.4426950408889634f;
   if (dm.d == 128)
     hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
                        (const uint16_t*)k, (const uint16_t*)v, w.trec, w.dp_start, w.sk_start, w.qmap,
-                       (uint16_t*)o, lse, w.part_o, w.part_m, w.part_l, gm, scale_log2);
+                       (uint16_t*)o, lse, w.part_o, w.part_m, w.part_l, gm, Tcap, scale_log2);
   else
     hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(P), dim3(kThreads), 0, st, (const uint16_t*)q,
                        (const uint16_t*)k, (const uint16_t*)v, w.trec, w.dp_start, w.sk_start, w.qmap,
-                       (uint16_t*)o, lse, w.part_o, w.part_m, w.part_l, gm, scale_log2);
+                       (uint16_t*)o, lse, w.part_o, w.part_m, w.part_l, gm, Tcap, scale_log2);
   return hipGetLastError();
 }
 
@@ -1118,10 +1132,12 @@ hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipS
   const dim3 cgrid(P, QR / kCombRows);
   if (dm.d == 128)
     hipLaunchKernelGGL(attn_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.ucount, w.sk_start, w.trec,
-                       w.qmap, P, row_tiles, dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
+                       w.qmap, P, dm.BH * row_tiles, (int)attn_tile_capacity(dm), row_tiles, dm.Lq, dm.block,
+                       w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   else
     hipLaunchKernelGGL(attn_combine_kernel<64>, cgrid, dim3(kCombThreads), 0, st, w.tstart, w.ucount, w.sk_start, w.trec,
-                       w.qmap, P, row_tiles, dm.Lq, dm.block, w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
+                       w.qmap, P, dm.BH * row_tiles, (int)attn_tile_capacity(dm), row_tiles, dm.Lq, dm.block,
+                       w.part_o, w.part_m, w.part_l, (uint16_t*)o, lse);
   return hipGetLastError();
 }
 
