@@ -157,8 +157,10 @@ la_status la_sparse_attn_fwd(const la_shape* shape, const void* q, const void* k
  *   one workgroup, and partial results (O, running max, sum) into ws for the others.
  * la_sparse_attn_merge: merges those partials into o and lse (the buffers given to the
  *   run; lse may be NULL if it was NULL there).
- * Plan, run and merge must follow each other on one stream with the same ws.
- * Arguments, alignment and errors as for la_sparse_attn_fwd. */
+ * Plan, run and merge must follow each other on one stream with the same ws, with no other
+ * call using that ws in between (a selection call overwrites the plan): a run on a plan the
+ * workspace no longer holds writes wrong values, though every access stays inside q, k, v, o,
+ * lse and ws.  Arguments, alignment and errors as for la_sparse_attn_fwd. */
 la_status la_sparse_attn_plan(const la_shape* shape, const int32_t* counts, const int32_t* idx,
                               void* ws, size_t ws_bytes, void* stream);
 la_status la_sparse_attn_run(const la_shape* shape, const void* q, const void* k, const void* v,
