@@ -210,7 +210,7 @@ def test_attn_plan_run_merge_equal_fwd():
     v2 = (g["v"].float() * -2.0).to(torch.bfloat16)
     o3 = la.sparse_attn_fwd(q2, g["k"], v2, counts, idx, block)
     run2, merge2 = la.bind_attn_steps(q2, g["k"], v2, counts, idx, block, o2, ws, lse=lse2)[1:]
-    for _ in range(3):      # the cut units' counters are back at zero after every run
+    for _ in range(3):      # one plan serves any number of runs
         o2.zero_()
         run2()
         merge2()
