@@ -267,7 +267,9 @@ def pool_blocks(x: torch.Tensor, block: int, which: str, shape: Shape, out: Opti
 def bind_attn_steps(q, k, v, counts, idx, block, o, ws, scale: Optional[float] = None, n_text: int = 0,
                     frame_tokens: int = 0, lse: Optional[torch.Tensor] = None):
     """(plan, run, merge) of la_sparse_attn_fwd as BoundCalls on fixed tensors and the current
-    stream; plan + run + merge computes the same o (and lse) as sparse_attn_fwd."""
+    stream; plan + run + merge computes the same o (and lse) as sparse_attn_fwd.  One plan serves
+    any number of runs, as long as no other call uses `ws` in between (a selection call writes
+    its scores there): after such a call, plan again before the next run."""
     _check_qkv("q", q)
     B, H, Lq, d = q.shape
     _check_qkv("k", k, B, H, d)
