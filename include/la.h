@@ -169,6 +169,26 @@ la_status la_sparse_attn_run(const la_shape* shape, const void* q, const void* k
 la_status la_sparse_attn_merge(const la_shape* shape, void* o, float* lse, void* ws,
                                size_t ws_bytes, void* stream);
 
+/* The schedule of the plan in ws, for tools and tests that check or study it; it changes
+ * nothing.  Units u < U = B H ceil(Lq / 256) own T tiles in all, ordered in one tile
+ * sequence; the run's P persistent workgroups (one per CU of the current device, a multiple
+ * of 8, at most 256) each take a range of whole units and a share cut anywhere.  Written:
+ *   *P, *U    (host)  the two counts the arrays below are sized by;
+ *   tstart    int32 [U + 1] (device): position of unit u's first tile; tstart[U] = T;
+ *   ucount    int32 [U]     (device): 64-key tiles of unit u's list union (a unit with 0 still
+ *             runs one tile, so it takes max(1, ucount[u]) positions);
+ *   dp_start  int32 [P + 1] (device): workgroup l runs the whole units on [dp_start[l],
+ *             dp_start[l + 1]) (rounds: its XCD's consecutive units);
+ *   sk_start  int32 [P + 1] (device): and its share [sk_start[l], sk_start[l + 1]) of the
+ *             remaining tiles, which starts at dp_start[P].
+ * Any of the four arrays may be NULL (not copied); the copies run on `stream`.  The values
+ * describe the plan la_sparse_attn_plan(_valid) built for `shape` on this device, as long as
+ * no other call has used ws since; otherwise they are meaningless.  LA_ERR_ARG if P or U is
+ * NULL; workspace errors as for la_sparse_attn_run. */
+la_status la_sparse_attn_schedule(const la_shape* shape, const void* ws, size_t ws_bytes,
+                                  int32_t* P, int32_t* U, int32_t* tstart, int32_t* ucount,
+                                  int32_t* dp_start, int32_t* sk_start, void* stream);
+
 /* Compacts a block mask (uint8 [B, H, NQ, NK], non-zero = kept) into the
  * counts/idx form la_sparse_attn_fwd reads.  Needs no workspace. */
 la_status la_mask_to_list(const la_shape* shape, const uint8_t* mask, int32_t* counts,

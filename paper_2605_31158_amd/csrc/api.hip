@@ -240,6 +240,21 @@ la_status la_sparse_attn_merge(const la_shape* shape, void* o, float* lse, void*
   return e == hipSuccess ? LA_OK : LA_ERR_HIP;
 }
 
+la_status la_sparse_attn_schedule(const la_shape* shape, const void* ws, size_t ws_bytes, int32_t* P,
+                                  int32_t* U, int32_t* tstart, int32_t* ucount, int32_t* dp_start,
+                                  int32_t* sk_start, void* stream) {
+  Dims dm;
+  la_status st = attn_check(shape, &dm, const_cast<void*>(ws), ws_bytes);
+  if (st != LA_OK) return st;
+  if (!P || !U) return LA_ERR_ARG;
+  int p = 0, u = 0;
+  hipError_t e = read_attn_schedule(dm, ws, tstart, ucount, dp_start, sk_start, &p, &u, (hipStream_t)stream);
+  if (e != hipSuccess) return LA_ERR_HIP;
+  *P = p;
+  *U = u;
+  return LA_OK;
+}
+
 la_status la_mask_to_list(const la_shape* shape, const uint8_t* mask, int32_t* counts, int32_t* idx,
                           void* stream) {
   Dims dm;

@@ -1141,4 +1141,23 @@ hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipS
   return hipGetLastError();
 }
 
+hipError_t read_attn_schedule(const Dims& dm, const void* ws, int32_t* tstart, int32_t* ucount, int32_t* dp_start,
+                              int32_t* sk_start, int* P, int* U, hipStream_t st) {
+  const AttnWs w = attn_ws_layout(dm, const_cast<void*>(ws));
+  *P = persistent_workgroups();
+  *U = dm.BH * ceil_div(dm.Lq, QR);
+  const struct {
+    int32_t* dst;
+    const int32_t* src;
+    int n;
+  } parts[4] = {{tstart, w.tstart, *U + 1}, {ucount, w.ucount, *U}, {dp_start, w.dp_start, *P + 1},
+                {sk_start, w.sk_start, *P + 1}};
+  for (const auto& c : parts) {
+    if (!c.dst) continue;
+    const hipError_t e = hipMemcpyAsync(c.dst, c.src, (size_t)c.n * sizeof(int32_t), hipMemcpyDeviceToDevice, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 }  // namespace la

@@ -54,6 +54,10 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
 hipError_t launch_attn_run(const Dims& dm, const void* q, const void* k, const void* v, float scale, void* o,
                            float* lse, void* ws, hipStream_t st);
 hipError_t launch_attn_merge(const Dims& dm, void* o, float* lse, void* ws, hipStream_t st);
+// Copies the schedule arrays of the plan in ws (any destination may be null) and reports the
+// persistent workgroup count P and the unit count U they are sized by.
+hipError_t read_attn_schedule(const Dims& dm, const void* ws, int32_t* tstart, int32_t* ucount, int32_t* dp_start,
+                              int32_t* sk_start, int* P, int* U, hipStream_t st);
 
 // The 3-D block layout of a la_grid3d: block counts, linear lengths and the tiled la_shape.
 struct G3Dims {

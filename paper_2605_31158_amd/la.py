@@ -59,6 +59,7 @@ _SIGNATURES = {
     "la_sparse_attn_plan": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_run": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_float, _P, _P, _P, ctypes.c_size_t, _P]),
     "la_sparse_attn_merge": (ctypes.c_int, [_SP, _P, _P, _P, ctypes.c_size_t, _P]),
+    "la_sparse_attn_schedule": (ctypes.c_int, [_SP, _P, ctypes.c_size_t, _P, _P, _P, _P, _P, _P, _P]),
     "la_mask_to_list": (ctypes.c_int, [_SP, _P, _P, _P, _P]),
     "la_grid3d_shape": (ctypes.c_int, [_GP, _SP]),
     "la_grid3d_valid": (ctypes.c_int, [_GP, _P, _P]),
@@ -287,6 +288,23 @@ def bind_attn_steps(q, k, v, counts, idx, block, o, ws, scale: Optional[float] =
     merge = BoundCall("la_sparse_attn_merge", ctypes.byref(shape), _ptr(o), _ptr(lse), _ptr(ws), nbytes, st,
                       keep=keep)
     return plan, run, merge
+
+
+def plan_schedule(shape: Shape, ws: torch.Tensor) -> dict:
+    """The schedule of the plan in ws (la_sparse_attn_schedule): P, U and the arrays tstart
+    [U+1], ucount [U], dp_start [P+1], sk_start [P+1] as int64 CPU tensors (synchronises)."""
+    P, U = ctypes.c_int32(0), ctypes.c_int32(0)
+    _call("la_sparse_attn_schedule", ctypes.byref(shape), _ptr(ws), ctypes.c_size_t(ws.numel()), ctypes.byref(P),
+          ctypes.byref(U), None, None, None, None, _stream(ws))
+    arrs = {"tstart": int(U.value) + 1, "ucount": int(U.value), "dp_start": int(P.value) + 1,
+            "sk_start": int(P.value) + 1}
+    bufs = {k: torch.empty(n, dtype=torch.int32, device=ws.device) for k, n in arrs.items()}
+    _call("la_sparse_attn_schedule", ctypes.byref(shape), _ptr(ws), ctypes.c_size_t(ws.numel()), ctypes.byref(P),
+          ctypes.byref(U), _ptr(bufs["tstart"]), _ptr(bufs["ucount"]), _ptr(bufs["dp_start"]),
+          _ptr(bufs["sk_start"]), _stream(ws))
+    out = {k: b.cpu().to(torch.int64) for k, b in bufs.items()}
+    out["P"], out["U"] = int(P.value), int(U.value)
+    return out
 
 
 def bind_select_cached(q, block, tau, kbar, qbar, mask, counts, idx, ws, Lk: int, n_text: int = 0):

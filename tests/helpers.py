@@ -91,3 +91,59 @@ def assert_attn_close(o_gpu, o_ref, what=""):
 def bf16_tensor_to_f64(t):
     import torch
     return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def check_schedule(s, row_tiles=None):
+    """Checks the schedule of an attention plan (la.plan_schedule) against the rule the library
+    states (include/la.h, la_sparse_attn_schedule): the units' tile ranges fill [0, T) without
+    overlap; workgroup l runs, on [dp_start[l], dp_start[l+1]), the units x R P/8 + r P/8 + c
+    (l = x P/8 + c, r < R = (U - P/4) / P) that are at most T / (P R) tiles long, in that order;
+    every other unit follows from dp_start[P] = T_dp on, in unit order; the shares
+    [sk_start[l], sk_start[l+1]) fill [T_dp, T); and no workgroup gets more than ceil(T/P)
+    tiles.  row_tiles (optional, [B*H, NQ]): the tiles of each query block's own list; the
+    tiles of a head's units then lie between the longest list and the sum of its lists.
+    Returns a summary (T, rounds, round tiles, largest and mean workgroup load)."""
+    P, U = int(s["P"]), int(s["U"])
+    ts = np.asarray(s["tstart"], np.int64)
+    uc = np.asarray(s["ucount"], np.int64)
+    dp = np.asarray(s["dp_start"], np.int64)
+    sk = np.asarray(s["sk_start"], np.int64)
+    assert ts.shape == (U + 1,) and uc.shape == (U,) and dp.shape == (P + 1,) and sk.shape == (P + 1,)
+    assert P >= 8 and P % 8 == 0 and P <= 256, P
+    assert (uc >= 0).all()
+    n = np.maximum(1, uc)
+    T = int(n.sum())
+    assert ts[U] == T, (ts[U], T)
+    order = np.argsort(ts[:U], kind="stable")
+    starts = ts[:U][order]
+    assert starts[0] == 0 and (starts[1:] == starts[:-1] + n[order][:-1]).all(), "unit ranges overlap or leave gaps"
+    R = (U - P // 4) // P if U > P // 4 else 0
+    PX = P // 8
+    thr = max(1, T // (P * R)) if R > 0 else 0
+    in_r = np.zeros(U, bool)
+    in_r[:R * P] = n[:R * P] <= thr
+    Tdp = int(n[in_r].sum())
+    assert dp[0] == 0 and dp[P] == Tdp and (np.diff(dp) >= 0).all(), "round ranges"
+    for lam in range(P):
+        pos = dp[lam]
+        for r in range(R):
+            u = (lam // PX) * R * PX + r * PX + lam % PX
+            if in_r[u]:
+                assert ts[u] == pos, (lam, r, u, ts[u], pos)
+                pos += n[u]
+        assert pos == dp[lam + 1], (lam, pos, dp[lam + 1])
+    pos = Tdp
+    for u in np.nonzero(~in_r)[0]:
+        assert ts[u] == pos, (u, ts[u], pos)
+        pos += n[u]
+    assert pos == T
+    assert sk[0] == Tdp and sk[P] == T and (np.diff(sk) >= 0).all(), "shares"
+    load = np.diff(dp) + np.diff(sk)
+    assert load.max() <= -(-T // P), (int(load.max()), T, P)
+    if row_tiles is not None:
+        rt = np.asarray(row_tiles, np.int64)
+        BH = rt.shape[0]
+        assert U % BH == 0
+        per_head = uc.reshape(BH, U // BH).sum(1)
+        assert (per_head >= rt.max(1)).all() and (per_head <= rt.sum(1)).all(), "unit tiles vs lists"
+    return {"T": T, "R": R, "T_rounds": Tdp, "max_load": int(load.max()), "mean_load": T / P}

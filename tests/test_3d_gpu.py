@@ -13,7 +13,7 @@ import torch
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
 from paper_2605_31158_amd.workloads import WORKLOADS_3D, Workload3D, make_inputs_3d
-from helpers import say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
+from helpers import check_schedule, say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -204,8 +204,14 @@ def test_valid_counts_mask_padding_and_full_counts_change_nothing():
     NQ, NK = shape.Lq // wl.block, shape.Lk // wl.block
     mask = torch.ones((wl.B, wl.H, NQ, NK), dtype=torch.uint8, device="cuda")
     counts, idx = la.mask_to_list(mask, wl.block, shape.Lq, shape.Lk, wl.d)
+    ws = torch.empty(la.workspace_bytes(shape), dtype=torch.uint8, device="cuda")
     o1, l1 = la.sparse_attn_fwd(q_t, k_t, v_t, counts, idx, wl.block, n_text=shape.n_text, want_lse=True,
-                                kvalid=kvalid)
+                                kvalid=kvalid, ws=ws)
+    # the plan leaves out the sub-tiles with no valid key: a key block of v valid keys has
+    # ceil(v / 64) tiles, and every query block keeps every key block here
+    kv = la.grid3d_valid(grid)[1].astype(np.int64)
+    per_row = int(sum(-(-min(wl.block, int(x)) // 64) for x in kv))
+    check_schedule(la.plan_schedule(shape, ws), row_tiles=np.full((wl.B * wl.H, NQ), per_row))
     # garbage in every padding slot: the valid counts keep it out
     pad = torch.from_numpy(la.grid3d_valid(grid)[1]).cuda()
     slot = torch.arange(shape.Lk, device="cuda") % wl.block

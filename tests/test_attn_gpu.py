@@ -11,7 +11,8 @@ import torch
 from oracle import la_oracle as O
 from paper_2605_31158_amd import la
 from paper_2605_31158_amd.workloads import WORKLOADS, CONFIG_ORDER, make_inputs, make_clustered
-from helpers import say, tau32, to_gpu, check_list, check_selection, assert_attn_close, bf16_tensor_to_f64
+from helpers import (say, tau32, to_gpu, check_list, check_selection, check_schedule, assert_attn_close,
+                     bf16_tensor_to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -27,6 +28,14 @@ def gpu_attn_on_mask(inp, mask_np, block, frame_tokens=0, n_text=0, scale=None):
                                 frame_tokens=frame_tokens, want_lse=True)
     torch.cuda.synchronize()
     return bf16_tensor_to_f64(o), lse.cpu().numpy().astype(np.float64)
+
+
+def row_tiles_1d(mask, block, Lk):
+    """64-key tiles of each query block's own list (a key block has ceil(valid keys / 64)):
+    [B*H, NQ]."""
+    B, H, NQ, NK = mask.shape
+    st = np.array([-(-min(block, Lk - j * block) // 64) for j in range(NK)], np.int64)
+    return mask.reshape(B * H, NQ, NK).astype(np.int64) @ st
 
 
 def compare(o, lse, o_ref, lse_ref, what):
@@ -123,10 +132,14 @@ def test_attn_named_workloads_on_gpu_mask(name):
     inp = make_inputs(wl)
     g = to_gpu(inp)
     mask, counts, idx = la.select_blocks(g["q"], g["k"], wl.block, wl.tau)
-    o, lse = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, wl.block, want_lse=True)
+    shape = la.make_shape(wl.B, wl.H, wl.Lq, wl.Lk, wl.d, wl.block)
+    ws = torch.empty(la.workspace_bytes(shape), dtype=torch.uint8, device="cuda")
+    o, lse = la.sparse_attn_fwd(g["q"], g["k"], g["v"], counts, idx, wl.block, want_lse=True, ws=ws)
     torch.cuda.synchronize()
     mask_np = mask.cpu().numpy()
     check_list(mask_np, counts.cpu().numpy(), idx.cpu().numpy())
+    info = check_schedule(la.plan_schedule(shape, ws), row_tiles=row_tiles_1d(mask_np, wl.block, wl.Lk))
+    say(f"[attn] {name}: schedule {info}")
     o = bf16_tensor_to_f64(o)
     lse = lse.cpu().numpy()
     B, H, NQ = wl.B, wl.H, wl.nq
@@ -268,3 +281,38 @@ def test_attn_rounds_long_units_and_empty_units():
         sl = {x: inp[x][b:b + 1, h:h + 1] for x in "qkv"}
         o_ref, lse_ref = O.attention(sl["q"], sl["k"], sl["v"], mask[b:b + 1, h:h + 1], block)
         compare(o[b:b + 1, h:h + 1], lse[b:b + 1, h:h + 1], o_ref, lse_ref, f"rounds head {bh}")
+
+
+SCHED = [
+    # B, H, Lq, Lk, d, block, density, dense heads, empty heads, label
+    (2, 320, 256, 2048, 64, 64, 0.2, 24, 24, "two rounds, long and empty units"),
+    (4, 128, 512, 3000, 64, 64, 0.1, 16, 8, "three rounds, ragged keys"),
+    (1, 64, 1024, 4096, 64, 128, 0.25, 4, 4, "no rounds, block 128"),
+    (1, 2, 300, 1000, 128, 64, 0.4, 0, 0, "few units"),
+    (1, 1, 1030 * 64 - 20, 1030 * 64 + 700, 64, 64, 0.05, 0, 0, "one head past the grouping limit"),
+]
+
+
+@pytest.mark.parametrize("case", SCHED, ids=[c[-1] for c in SCHED])
+def test_attn_schedule_invariants(case):
+    # the plan's schedule follows the stated rule (whole units in XCD-major rounds, long units
+    # demoted, shares within ceil(T / P) tiles per workgroup), read back from the workspace
+    B, H, Lq, Lk, d, block, density, n_dense, n_empty, label = case
+    say(f"[sched] {label}: B={B} H={H} Lq={Lq} Lk={Lk} d={d} block={block}")
+    rng = np.random.default_rng(B * H + Lq)
+    NQ, NK = -(-Lq // block), -(-Lk // block)
+    mask = (rng.uniform(size=(B, H, NQ, NK)) < density).astype(np.uint8)
+    flat = mask.reshape(B * H, NQ, NK)
+    heads = rng.permutation(B * H)
+    flat[heads[:n_dense]] = 1
+    flat[heads[n_dense:n_dense + n_empty]] = 0
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    q = torch.randn((B, H, Lq, d), device="cuda", generator=gen).to(torch.bfloat16)
+    k = torch.randn((B, H, Lk, d), device="cuda", generator=gen).to(torch.bfloat16)
+    v = torch.randn((B, H, Lk, d), device="cuda", generator=gen).to(torch.bfloat16)
+    counts, idx = la.mask_to_list(torch.from_numpy(mask).cuda(), block, Lq, Lk, d)
+    shape = la.make_shape(B, H, Lq, Lk, d, block)
+    ws = torch.empty(la.workspace_bytes(shape), dtype=torch.uint8, device="cuda")
+    la.sparse_attn_fwd(q, k, v, counts, idx, block, ws=ws)
+    info = check_schedule(la.plan_schedule(shape, ws), row_tiles=row_tiles_1d(mask, block, Lk))
+    say(f"[sched] {label}: {info}")
