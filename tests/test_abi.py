@@ -76,6 +76,9 @@ def test_bad_shapes_rejected(bad):
     assert lib.la_sparse_attn_run(ctypes.byref(s), p, p, p, ctypes.c_float(0), p, None, p, 1 << 30,
                                   None) == la.LA_ERR_SHAPE
     assert lib.la_sparse_attn_merge(ctypes.byref(s), p, None, p, 1 << 30, None) == la.LA_ERR_SHAPE
+    n = ctypes.c_int32(0)
+    assert lib.la_sparse_attn_schedule(ctypes.byref(s), p, 1 << 30, ctypes.byref(n), ctypes.byref(n), p, p, p, p,
+                                       None) == la.LA_ERR_SHAPE
 
 
 @cpu_only
@@ -125,6 +128,14 @@ def test_bad_arguments_rejected():
     assert lib.la_pool_blocks(ctypes.byref(s), None, 0, p, None) == la.LA_ERR_ARG
     assert lib.la_pool_blocks(ctypes.byref(s), p, 1, odd, None) == la.LA_ERR_ARG
     assert lib.la_sparse_attn_merge(ctypes.byref(s), odd, None, p, ws, None) == la.LA_ERR_ARG
+    sch = lib.la_sparse_attn_schedule
+    n = ctypes.c_int32(-5)
+    assert sch(ctypes.byref(s), p, ws, None, ctypes.byref(n), p, p, p, p, None) == la.LA_ERR_ARG
+    assert sch(ctypes.byref(s), p, ws, ctypes.byref(n), None, p, p, p, p, None) == la.LA_ERR_ARG
+    assert sch(ctypes.byref(s), None, ws, ctypes.byref(n), ctypes.byref(n), p, p, p, p, None) == la.LA_ERR_WORKSPACE
+    assert sch(ctypes.byref(s), p, 16, ctypes.byref(n), ctypes.byref(n), p, p, p, p, None) == la.LA_ERR_WORKSPACE
+    assert sch(None, p, ws, ctypes.byref(n), ctypes.byref(n), p, p, p, p, None) == la.LA_ERR_ARG
+    assert n.value == -5                 # nothing written on an error
 
 
 @cpu_only
