@@ -8,7 +8,8 @@
 //                 whole blocks into LDS (never written out), then the workgroup scores the
 //                 G pooled keys against every pooled query of the head with fp32 MFMA
 //                 (v_mfma_f32_16x16x4_f32) -> s fp32 [BH, NQ, M] (workspace).  The K read is
-//                 the dominant cost of selection; it is one coalesced streaming pass.
+//                 the dominant cost of selection; it is one coalesced streaming pass of
+//                 non-temporal loads.
 //   select_rows   one wave per (head, query block), no workgroup barriers: softmax over the
 //                 M scores, then a radix select over the 32-bit order keys of the scores (4
 //                 passes of 8 bits, per-wave LDS histogram) that finds the score at which the
@@ -39,7 +40,9 @@ __device__ inline void acc_bf16x8(float* a, u32x4 w) {
 // Sums the `rows` valid rows of one block (rows x D bf16, row-major at `base`) with one wave.
 // Lane l owns 16-byte chunk l % CH of rows l / CH + RG * r; every lane's loads are issued
 // before any is consumed.  On return every lane holds the column sums of its chunk (8 floats).
-template <int D, int BLOCK>
+// NT: non-temporal loads, for data read once per call (the historical keys, hundreds of MB):
+// the stream then does not displace what the caches hold for the passes that follow.
+template <int D, int BLOCK, bool NT = false>
 __device__ inline void wave_block_sum(const uint16_t* __restrict__ base, int rows, float* a) {
   constexpr int CH = D / 8;           // chunks per row
   constexpr int RG = 64 / CH;         // row groups per wave
@@ -55,7 +58,8 @@ __device__ inline void wave_block_sum(const uint16_t* __restrict__ base, int row
 #pragma unroll
     for (int u = 0; u < BATCH; ++u) {
       const int r = rg + RG * (b0 + u);
-      w[u] = r < rows ? *(const u32x4*)(base + (size_t)r * D + ch * 8) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4* p = (const u32x4*)(base + (size_t)r * D + ch * 8);
+      w[u] = r >= rows ? u32x4{0u, 0u, 0u, 0u} : NT ? __builtin_nontemporal_load(p) : *p;
     }
 #pragma unroll
     for (int u = 0; u < BATCH; ++u) acc_bf16x8(a, w[u]);
@@ -131,7 +135,7 @@ __global__ __launch_bounds__(kScoreThreads) void pool_k_score_kernel(const void*
     } else if (g < gcount) {
       const int j = h0 + m0 + g;   // historical blocks are whole: no ragged rows
       float a[8];
-      wave_block_sum<D, BLOCK>(k + ((size_t)bh * Lk + (size_t)j * BLOCK) * D, BLOCK, a);
+      wave_block_sum<D, BLOCK, true>(k + ((size_t)bh * Lk + (size_t)j * BLOCK) * D, BLOCK, a);
       if (lane < CH) {
         *(f32x4*)&kb[g][lane * 8] = f32x4{a[0] * inv_block, a[1] * inv_block, a[2] * inv_block, a[3] * inv_block};
         *(f32x4*)&kb[g][lane * 8 + 4] = f32x4{a[4] * inv_block, a[5] * inv_block, a[6] * inv_block, a[7] * inv_block};
