@@ -55,8 +55,9 @@ __device__ inline double block_sum(double x) {
 }
 
 // Pass 1: chunk c (16 bytes) goes to thread (c mod G) of the grid, G = gridDim.x threads per
-// block times blocks; each lane has UNROLL chunk loads in flight.  The n % W trailing values
-// (W values per chunk) are added by the first threads of workgroup 0.
+// block times blocks; each lane has UNROLL chunk loads in flight (non-temporal: both latents are
+// read once).  The n % W trailing values (W values per chunk) are added by the first threads of
+// workgroup 0.
 template <bool BF16>
 __global__ __launch_bounds__(kMseThreads) void mse_partial_kernel(const void* __restrict__ a,
                                                                   const void* __restrict__ b, int64_t n,
@@ -74,8 +75,8 @@ __global__ __launch_bounds__(kMseThreads) void mse_partial_kernel(const void* __
     u32x4 x[UNROLL], y[UNROLL];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      x[u] = va[c + u * G];
-      y[u] = vb[c + u * G];
+      x[u] = __builtin_nontemporal_load(va + c + u * G);
+      y[u] = __builtin_nontemporal_load(vb + c + u * G);
     }
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) acc += (double)chunk_sq<BF16>(x[u], y[u]);

@@ -8,7 +8,10 @@
 // block-major side is one contiguous span.
 //   prep_kernel<NSRC = 1>  Q-Prep: chunk queries -> block-major Q, and the block means q_bar.
 //   prep_kernel<NSRC = 2>  KV-Prep: K and V of one region (text, context or chunk) -> block-major
-//                          K and V, and the block means k_bar of K.  One launch per region.
+//                          K and V, and the block means k_bar of K.  One launch per region; the
+//                          context region (read once per AR chunk, the bulk of the bytes) is read
+//                          with non-temporal loads, so its stream does not displace the cached
+//                          data of the passes that follow.
 //   untile_kernel          block-major O (and lse) -> linear order, padding slots dropped.
 // Means are sums of the bf16 values in fp32 over the block's valid tokens, then one multiply by
 // 1 / count; padding slots load as zero and add nothing.
@@ -89,8 +92,8 @@ __device__ inline void slot_tokens(const Grid3& g, const BlockMap& bm, int* tok)
 
 // Lane layout: chunk c = tid % CH (16 bytes of a row), slot tid / CH + RPP p for pass p.  The
 // loads are unconditional (padding slots read the block's first token and are zeroed), so all
-// NP (K: and NP V) loads of a lane are in flight before the first store.
-template <int D, int BLOCK, int NSRC>
+// NP (K: and NP V) loads of a lane are in flight before the first store.  NT: non-temporal loads.
+template <int D, int BLOCK, int NSRC, bool NT = false>
 __global__ __launch_bounds__(kTileThreads) void prep_kernel(const uint16_t* __restrict__ src0,
                                                             const uint16_t* __restrict__ src1,
                                                             uint16_t* __restrict__ dst0, uint16_t* __restrict__ dst1,
@@ -110,8 +113,12 @@ __global__ __launch_bounds__(kTileThreads) void prep_kernel(const uint16_t* __re
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     const int off = tok[r0 + RPP * p] * D;
-    a[p] = *(const u32x4*)(s0 + off);
-    if constexpr (NSRC == 2) b[p] = *(const u32x4*)(s1 + off);
+    const u32x4* pa = (const u32x4*)(s0 + off);
+    a[p] = NT ? __builtin_nontemporal_load(pa) : *pa;
+    if constexpr (NSRC == 2) {
+      const u32x4* pb = (const u32x4*)(s1 + off);
+      b[p] = NT ? __builtin_nontemporal_load(pb) : *pb;
+    }
   }
   const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
@@ -250,24 +257,32 @@ hipError_t launch_prep_kv(const G3Dims& gd, const void* k, const void* v, uint32
   const Grid3 g = grid3(gd, gd.Lk_lin, gd.NK * gd.block, gd.NK);
   Run runs[3];
   int nblk[3], nr = 0;
+  bool stream[3];
   if ((parts & LA_PART_TEXT) && gd.NT > 0) {
     runs[nr] = Run{0, 0, 0, gd.n_text};
+    stream[nr] = false;
     nblk[nr++] = gd.NT;
   }
   if ((parts & LA_PART_CONTEXT) && gd.NC > 0) {
     runs[nr] = Run{gd.NT, gd.n_text, gd.T_ctx, 0};
+    stream[nr] = true;
     nblk[nr++] = gd.NC;
   }
   if (parts & LA_PART_CHUNK) {
     runs[nr] = Run{gd.NT + gd.NC, gd.n_text + gd.T_ctx * gd.F, gd.T_q, 0};
+    stream[nr] = false;
     nblk[nr++] = gd.NQ;
   }
   for (int i = 0; i < nr; ++i) {
     const dim3 grid(nblk[i], gd.BH);
     const Run run = runs[i];
     const bool ok = dispatch(gd.d, gd.block, [&](auto D, auto BLOCK) {
-      hipLaunchKernelGGL((prep_kernel<D(), BLOCK(), 2>), grid, dim3(kTileThreads), 0, st, (const uint16_t*)k,
-                         (const uint16_t*)v, (uint16_t*)k_tiled, (uint16_t*)v_tiled, kbar, g, run);
+      if (stream[i])
+        hipLaunchKernelGGL((prep_kernel<D(), BLOCK(), 2, true>), grid, dim3(kTileThreads), 0, st, (const uint16_t*)k,
+                           (const uint16_t*)v, (uint16_t*)k_tiled, (uint16_t*)v_tiled, kbar, g, run);
+      else
+        hipLaunchKernelGGL((prep_kernel<D(), BLOCK(), 2>), grid, dim3(kTileThreads), 0, st, (const uint16_t*)k,
+                           (const uint16_t*)v, (uint16_t*)k_tiled, (uint16_t*)v_tiled, kbar, g, run);
       return true;
     });
     if (!ok) return hipErrorInvalidValue;
