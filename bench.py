@@ -4,7 +4,11 @@
 A step is one pass of the whole path over one synthetic batch already resident in HBM:
 la_select_blocks (pool Q, pool+score historical K, select and compact) followed by the three
 steps of la_sparse_attn_fwd over the kept blocks (plan, run, merge), each called through its own
-entry point so that HIP events on the launch stream time every stage.  Prints ONE JSON line.
+entry point so that HIP events on the launch stream can time every stage.  Prints ONE JSON line.
+
+The K timed steps carry HIP events only around the attention kernel (the run stage), for its
+roofline: every event record costs the GPU about 3 us, which with one event per stage added 4 % to
+a 480P step.  The per-stage times come from K more steps, with an event between every two stages.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
@@ -108,6 +112,39 @@ def clock_warmup(stages, ms: float):
         n += 8
         torch.cuda.synchronize()
     return n, round((time.perf_counter() - t0) * 1e3, 1)
+
+
+def timed_steps(stages, run_index: int, stream, K: int):
+    """The timed region: K steps between two device synchronisations, HIP events only around stage
+    run_index (the attention kernel).  Returns (wall ms per step, event ms of that stage per step)."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for it in range(K):
+        for j, f in enumerate(stages):
+            if j == run_index:
+                ev[it][0].record(stream)
+            f()
+            if j == run_index:
+                ev[it][1].record(stream)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / K
+    return ms_step, np.array([a.elapsed_time(b) for a, b in ev])
+
+
+def stage_times(stages, stream, K: int):
+    """K more steps with a HIP event between every two stages: ms per stage, [K, len(stages)]."""
+    import torch
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(K)]
+    torch.cuda.synchronize()
+    for it in range(K):
+        ev[it][0].record(stream)
+        for j, f in enumerate(stages):
+            f()
+            ev[it][j + 1].record(stream)
+    torch.cuda.synchronize()
+    return np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(len(stages))] for i in range(K)])
 
 
 def kept_flop_count(mask_np, Lq: int, Lk: int, block: int, d: int) -> int:
@@ -252,7 +289,8 @@ def cpu_baseline_3d(wl, inp, mask_np, qvalid, kvalid, target_s: float):
 
 def main_3d(args, wl):
     """The 3-D block path: Q-Prep, KV-Prep, selection from the pooled means, attention (plan, run,
-    merge) over the block-major buffers, Untile Scatter; each stage timed with HIP events."""
+    merge) over the block-major buffers, Untile Scatter; the attention kernel timed with HIP events
+    in the timed steps, every stage in a second loop."""
     import torch
     from paper_2605_31158_amd import la
     from paper_2605_31158_amd.workloads import make_inputs_3d
@@ -294,17 +332,10 @@ def main_3d(args, wl):
             f()
     torch.cuda.synchronize()
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(K)]
-    t0 = time.perf_counter()
-    for it in range(K):
-        ev[it][0].record(stream)
-        for j, f in enumerate(stages):
-            f()
-            ev[it][j + 1].record(stream)
-    torch.cuda.synchronize()
-    ms_step = (time.perf_counter() - t0) * 1e3 / K
-    st_ms = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(len(stages))] for i in range(K)])
+    ms_step, t_run = timed_steps(stages, names.index("attn_run"), stream, K)
+    st_ms = stage_times(stages, stream, K)
     t = {n: float(np.mean(st_ms[:, j])) for j, n in enumerate(names)}
+    t["attn_run"] = float(np.mean(t_run))
 
     mask_np = mask.cpu().numpy()
     kept_flops = float(kept_flop_count_3d(mask_np, qv, kv, d))
@@ -444,20 +475,10 @@ def main():
             f()
     torch.cuda.synchronize()
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for it in range(K):
-        ev[it][0].record(stream)
-        for j, f in enumerate(stages):
-            f()
-            ev[it][j + 1].record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / K
-    st_ms = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(len(stages))] for i in range(K)])
-    t_sel, t_plan, t_run, t_merge = (st_ms[:, j] for j in range(4))
-    t_att = t_plan + t_run + t_merge
+    ms_step, t_run = timed_steps(stages, 2, stream, K)
+    st_ms = stage_times(stages, stream, K)
+    t_sel, t_plan, t_run_b, t_merge = (st_ms[:, j] for j in range(4))
+    t_att = t_plan + t_run_b + t_merge
 
     mask_np = mask.cpu().numpy()
     kept_flops = float(kept_flop_count(mask_np, Lq, wl.Lk, wl.block, d))
