@@ -493,9 +493,16 @@ hipError_t launch_rows(const Dims& dm, const float* scores, float tau, int keep_
 #define LA_SELECT(NPER)                                                                                      \
   hipLaunchKernelGGL(select_rows_kernel<NPER>, grid, dim3(kThreads), 0, st, scores, dm.NQ, dm.NK, dm.M, dm.h0, \
                      dm.h1, tau, keep_fixed, mask, counts, idx)
+  // candidates per lane: the smallest instantiation that holds the row (every phase of the
+  // kernel loops over all NPER slots of a lane)
   if (dm.M <= 64 * 4) LA_SELECT(4);
+  else if (dm.M <= 64 * 8) LA_SELECT(8);
+  else if (dm.M <= 64 * 12) LA_SELECT(12);
   else if (dm.M <= 64 * 16) LA_SELECT(16);
+  else if (dm.M <= 64 * 20) LA_SELECT(20);
+  else if (dm.M <= 64 * 25) LA_SELECT(25);
   else if (dm.M <= 64 * 32) LA_SELECT(32);
+  else if (dm.M <= 64 * 48) LA_SELECT(48);
   else LA_SELECT(64);
 #undef LA_SELECT
   return hipGetLastError();

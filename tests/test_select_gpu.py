@@ -1,5 +1,6 @@
 """GPU block selection vs the fp64 oracle: bit-exact mask outside the ambiguity band,
 counts and lists consistent with the mask, and a valid selection everywhere."""
+import functools
 import math
 
 import numpy as np
@@ -51,6 +52,34 @@ EDGE = [
     (1, 1, 64, 64 * 4097, 64, 64, 0, 0.95, 10, "M = 4096 (largest)"),
     (1, 4, 300, 64 * 700, 128, 64, 0, 0.99, 11, "M = 695, peaky"),
 ]
+
+
+# Row widths on both sides of every per-lane size of the row kernel (4, 8, 12, 16, 20, 25, 32, 48
+# and 64 candidates per lane), under both rules.
+ROW_WIDTHS = [256, 257, 512, 513, 768, 769, 1024, 1025, 1280, 1281, 1600, 1601, 2048, 2049, 3072, 3073]
+
+
+@functools.lru_cache(maxsize=2)
+def _width_inputs(M):
+    Lq, block = 128, 64
+    return make_clustered(1, 2, Lq, Lq + block * M, 64, block, 40 + M % 97)
+
+
+@pytest.mark.parametrize("rule", ["tau", "topk"])
+@pytest.mark.parametrize("M", ROW_WIDTHS)
+def test_select_every_row_width(M, rule):
+    block = 64
+    say(f"[select-width] M={M} rule={rule}")
+    inp = _width_inputs(M)
+    if rule == "tau":
+        mask, counts, idx = run_select(inp, block, tau=0.9)
+        sel = O.select_blocks(inp["q"], inp["k"], block, tau=tau32(0.9))
+    else:
+        keep = int(np.floor(0.175 * M + 1e-9))
+        mask, counts, idx = run_select(inp, block, keep=keep)
+        sel = O.select_blocks(inp["q"], inp["k"], block, topk_r=0.175)
+    check_selection(mask, sel)
+    check_list(mask, counts, idx)
 
 
 @pytest.mark.parametrize("case", EDGE, ids=[c[-1] for c in EDGE])
