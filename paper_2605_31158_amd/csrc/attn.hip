@@ -7,7 +7,7 @@
 //     which chose the same context share a unit.  Its tiles are the 64-key sub-tiles of the
 //     union of its blocks' kept lists, in ascending key order, each tagged with which of the
 //     unit's blocks kept it.
-//   * A planner (three small kernels) computes the grouping, every unit's union list, the
+//   * A planner (two small kernels) computes the grouping, every unit's union list, the
 //     schedule and one record per tile (first key, head, unit, ownership) in the tile sequence.
 //     One persistent workgroup per CU runs, first, whole units handed out in rounds: in each
 //     round the workgroups of one XCD start consecutive units of the same head together, so
@@ -485,12 +485,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_union_kernel(const int32_t*
 //     possible to T / P.  Units cut at these boundaries are merged afterwards.
 // R = (U - P / 4) / P leaves at least P / 4 units to the second part (when U >= P / 4), which
 // absorbs the differences in unit length.  tstart[u] = first tile of unit u; tstart[U] = T.
-// One workgroup of kPlanThreads >= P threads.
-__global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t* __restrict__ ucount, int U, int P,
-                                                                  int32_t* __restrict__ tstart,
-                                                                  int32_t* __restrict__ dp_start,
-                                                                  int32_t* __restrict__ sk_start) {
-  __shared__ int sh[kPlanThreads / 64];
+// Computed by one whole workgroup of kPlanThreads >= P threads (sh: its scan scratch); with
+// `all` it writes tstart, dp_start and sk_start, and in any case the placing thread writes the
+// first tile of unit `me` to *me_start (read after the workgroup's next barrier).
+__device__ void schedule_units(const int32_t* __restrict__ ucount, int U, int P, int me, bool all,
+                               int32_t* __restrict__ tstart, int32_t* __restrict__ dp_start,
+                               int32_t* __restrict__ sk_start, int* sh, int* me_start) {
   const int tid = threadIdx.x;
   const int PX = P >> 3;
   const int R = U > P / 4 ? (U - P / 4) / P : 0;
@@ -517,17 +517,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t*
   int Tdp;
   const int dpa = block_excl_scan_i(dp, sh, &Tdp);
   if (tid < P) {
-    dp_start[tid] = dpa;
+    if (all) dp_start[tid] = dpa;
     int pos = dpa;
     for (int r = 0; r < R; ++r) {
       const int u = round_unit(tid, r);
       if (in_rounds(u)) {
-        tstart[u] = pos;
+        if (all) tstart[u] = pos;
+        if (u == me) *me_start = pos;
         pos += tiles(u);
       }
     }
   }
-  if (tid == 0) dp_start[P] = Tdp;
+  if (all && tid == 0) dp_start[P] = Tdp;
   // units of the second part, in unit order after the round units
   int skp = 0;
   for (int u = u_lo; u < u_hi; ++u)
@@ -536,9 +537,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t*
   int pos = Tdp + block_excl_scan_i(skp, sh, &Tsk_sum);
   for (int u = u_lo; u < u_hi; ++u)
     if (!in_rounds(u)) {
-      tstart[u] = pos;
+      if (all) tstart[u] = pos;
+      if (u == me) *me_start = pos;
       pos += tiles(u);
     }
+  if (!all) return;
   const int Tsk = T - Tdp;
   if (tid == 0) tstart[U] = T;
   // second-part shares: quota q = max(0, ceil(T / P) - round tiles), scaled to the Tsk tiles
@@ -550,20 +553,28 @@ __global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t*
   if (tid == 0) sk_start[P] = T;
 }
 
-// Expands unit u's union list into one record per 64-key tile at its place tstart[u] in the
-// tile sequence.  With kvalid (valid keys at the front of each key block), a tile's padding keys
-// are counted into its flags.
+// Expands unit u's union list into one record per 64-key tile at its place in the tile
+// sequence.  Every workgroup computes the schedule (above) for its own unit; workgroup 0 also
+// writes tstart, dp_start and sk_start for the run and the merge.  With kvalid (valid keys at the
+// front of each key block), a tile's padding keys are counted into its flags.
 __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t* __restrict__ ulist,
                                                                   const int32_t* __restrict__ ucount,
-                                                                  const int32_t* __restrict__ kvalid,
-                                                                  const int32_t* __restrict__ tstart, int NK,
+                                                                  const int32_t* __restrict__ kvalid, int U,
+                                                                  int P, int32_t* __restrict__ tstart,
+                                                                  int32_t* __restrict__ dp_start,
+                                                                  int32_t* __restrict__ sk_start, int NK,
                                                                   int block, int row_tiles, int4* __restrict__ trec) {
+  __shared__ int sh[kPlanThreads / 64];
+  __shared__ int first_tile;
   const int u = blockIdx.x;
   const int tid = threadIdx.x;
+  if (tid == 0) first_tile = 0;
+  schedule_units(ucount, U, P, u, u == 0, tstart, dp_start, sk_start, sh, &first_tile);
+  __syncthreads();
   const int nt = ucount[u], n = nt > 0 ? nt : 1;
   const int nsub = block / KT;
   const int bh = u / row_tiles;
-  int4* out = trec + tstart[u];
+  int4* out = trec + first_tile;
   const int32_t* ul = ulist + (size_t)u * NK * nsub;
   for (int a = tid; a < n; a += kPlanThreads) {
     int key0 = 0, bits = 0;
@@ -1100,10 +1111,8 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
                      st, counts, idx, kvalid, dm.NQ, dm.NK, dm.h0, dm.h1, dm.Lk, dm.block, row_tiles, w.qmap,
                      w.ulist, w.ucount);
-  hipLaunchKernelGGL(plan_sched_kernel, dim3(1), dim3(kPlanThreads), 0, st, w.ucount, U, persistent_workgroups(),
-                     w.tstart, w.dp_start, w.sk_start);
-  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, w.tstart,
-                     dm.NK, dm.block, row_tiles, w.trec);
+  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U,
+                     persistent_workgroups(), w.tstart, w.dp_start, w.sk_start, dm.NK, dm.block, row_tiles, w.trec);
   return hipGetLastError();
 }
 
