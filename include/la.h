@@ -31,6 +31,12 @@
  *     LA_ERR_HIP reports a failed kernel launch (outputs are then undefined).
  *   - No floating-point atomics: results are bit-reproducible run to run.
  *   - Calls are thread-safe (no global state).
+ *   - The selection and attention calls enqueue kernel launches only (no memset,
+ *     copy, allocation or synchronisation), so a caller may capture them in a
+ *     HIP graph; replays give the same results as the calls.  Exceptions:
+ *     la_sparse_attn_schedule (a reading tool) enqueues copies, and the first
+ *     la_select_blocks_noalloc call on a device looks up its scratch address
+ *     (make that call before capturing).
  */
 #ifndef LA_H_
 #define LA_H_
