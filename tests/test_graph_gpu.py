@@ -78,3 +78,55 @@ def test_step_graph_replays_equal_eager(case):
             f()
     s.synchronize()
     assert torch.equal(o, ref[2])
+
+
+def test_3d_path_graph_replays_equal_eager():
+    # the 3-D path: Q-Prep, KV-Prep, selection from the pooled means, plan, run, merge, Untile
+    # Scatter, captured together (the tiny 3-D workload: text, ragged grid edges, padding slots)
+    from paper_2605_31158_amd.workloads import WORKLOADS_3D, make_inputs_3d
+    wl = WORKLOADS_3D["tiny_3d"]
+    inp = make_inputs_3d(wl)
+    g = to_gpu(inp)
+    grid = la.grid3d(wl.B, wl.H, wl.d, wl.n_text, wl.T_ctx, wl.T_q, wl.Hs, wl.Ws, wl.bt, wl.bh, wl.bw, wl.block)
+    shape = la.grid3d_shape(grid)
+    kvalid = torch.from_numpy(la.grid3d_valid(grid)[1]).cuda()
+    B, H, d, blk = wl.B, wl.H, wl.d, wl.block
+    NQ, NK = shape.Lq // blk, shape.Lk // blk
+    say(f"[graph] 3-D tiny: NQ={NQ} NK={NK}")
+    dev = "cuda"
+    q_t = torch.empty((B, H, shape.Lq, d), dtype=torch.bfloat16, device=dev)
+    k_t = torch.empty((B, H, shape.Lk, d), dtype=torch.bfloat16, device=dev)
+    v_t = torch.empty_like(k_t)
+    qbar = torch.empty((B, H, NQ, d), dtype=torch.float32, device=dev)
+    kbar = torch.empty((B, H, NK, d), dtype=torch.float32, device=dev)
+    mask = torch.empty((B, H, NQ, NK), dtype=torch.uint8, device=dev)
+    counts = torch.empty((B, H, NQ), dtype=torch.int32, device=dev)
+    idx = torch.empty((B, H, NQ, NK), dtype=torch.int32, device=dev)
+    o_t = torch.empty_like(q_t)
+    lse_t = torch.empty((B, H, shape.Lq), dtype=torch.float32, device=dev)
+    o = torch.empty_like(g["q"])
+    lse = torch.empty((B, H, g["q"].shape[2]), dtype=torch.float32, device=dev)
+    ws = torch.empty(la.workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        steps = la.bind_3d(grid, g["q"], g["k"], g["v"], q_t, k_t, v_t, qbar, kbar, mask, counts, idx, kvalid, o_t,
+                           lse_t, o, lse, ws, tau=wl.tau)
+        for _ in range(2):
+            for f in steps:
+                f()
+    s.synchronize()
+    ref = [t.clone() for t in (mask, o, lse)]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        for f in steps:
+            f()
+    s.synchronize()
+    for r in range(3):
+        with torch.cuda.stream(s):
+            for t in (mask, o, lse, o_t, q_t):
+                t.zero_()
+            graph.replay()
+        s.synchronize()
+        same = [torch.equal(a, b) for a, b in zip((mask, o, lse), ref)]
+        say(f"[graph] 3-D tiny: replay {r}: mask/o/lse equal {same}")
+        assert all(same)
