@@ -1,7 +1,8 @@
-"""The whole path (select, plan, run, merge) captured in one HIP graph: every replay equals the
-eager result bit for bit.  The calls record only kernel launches (no memset, copy, allocation or
-synchronisation), so a caller can capture them; the replays alternate with eager work that
-clears the outputs, as a serving loop would."""
+"""Serving-style use of the library: the whole path (select, plan, run, merge; and the 3-D path)
+captured in one HIP graph, where every replay equals the eager result bit for bit (the calls
+record only kernel launches: no memset, copy, allocation or synchronisation; the replays
+alternate with eager work that clears the outputs, as a serving loop would), and two problems in
+flight at once on two streams, each equal to its sequential run (no shared state)."""
 import numpy as np
 import pytest
 import torch
@@ -130,3 +131,47 @@ def test_3d_path_graph_replays_equal_eager():
         same = [torch.equal(a, b) for a, b in zip((mask, o, lse), ref)]
         say(f"[graph] 3-D tiny: replay {r}: mask/o/lse equal {same}")
         assert all(same)
+
+
+def test_two_streams_concurrently_equal_sequential():
+    # two different problems in flight at once on two streams (default priority), each with its
+    # own workspace: the library keeps no shared state, so each result equals its sequential run
+    probs = []
+    for spec in ((1, 4, 900, 4000, 128, 64, 0.9, 31), (2, 3, 600, 3000, 64, 128, 0.85, 32)):
+        B, H, Lq, Lk, d, block, tau, seed = spec
+        inp = make_clustered(B, H, Lq, Lk, d, block, seed)
+        g = to_gpu(inp)
+        NQ, NK = la.nblocks(Lq, block), la.nblocks(Lk, block)
+        shape = la.make_shape(B, H, Lq, Lk, d, block)
+        bufs = dict(ws=torch.empty(la.workspace_bytes(shape), dtype=torch.uint8, device="cuda"),
+                    mask=torch.empty((B, H, NQ, NK), dtype=torch.uint8, device="cuda"),
+                    counts=torch.empty((B, H, NQ), dtype=torch.int32, device="cuda"),
+                    idx=torch.empty((B, H, NQ, NK), dtype=torch.int32, device="cuda"),
+                    o=torch.empty_like(g["q"]),
+                    lse=torch.empty((B, H, Lq), dtype=torch.float32, device="cuda"))
+        probs.append((g, block, tau, bufs, torch.cuda.Stream()))
+    steps = []
+    for g, block, tau, b, s in probs:
+        with torch.cuda.stream(s):
+            steps.append(bound_step(g["q"], g["k"], g["v"], block, tau, b["mask"], b["counts"], b["idx"], b["o"],
+                                    b["lse"], b["ws"]))
+    refs = []
+    for (g, block, tau, b, s), st in zip(probs, steps):      # one after the other
+        with torch.cuda.stream(s):
+            for f in st:
+                f()
+        s.synchronize()
+        refs.append((b["mask"].clone(), b["o"].clone(), b["lse"].clone()))
+    for rep in range(3):                                      # both in flight, interleaved launches
+        for (g, block, tau, b, s) in probs:
+            with torch.cuda.stream(s):
+                b["o"].zero_()
+                b["mask"].zero_()
+        torch.cuda.synchronize()
+        for j in range(4):
+            for st in steps:
+                st[j]()
+        torch.cuda.synchronize()
+        for (g, block, tau, b, s), (rm, ro, rl) in zip(probs, refs):
+            assert torch.equal(b["mask"], rm) and torch.equal(b["o"], ro) and torch.equal(b["lse"], rl)
+    say("[streams] two problems in flight on two streams: equal to their sequential runs")
