@@ -7,7 +7,7 @@
 //     which chose the same context share a unit.  Its tiles are the 64-key sub-tiles of the
 //     union of its blocks' kept lists, in ascending key order, each tagged with which of the
 //     unit's blocks kept it.
-//   * A planner (two small kernels) computes the grouping, every unit's union list, the
+//   * A planner (two or three small kernels) computes the grouping, every unit's union list, the
 //     schedule and one record per tile (first key, head, unit, ownership) in the tile sequence.
 //     One persistent workgroup per CU runs, first, whole units handed out in rounds: in each
 //     round the workgroups of one XCD start consecutive units of the same head together, so
@@ -553,14 +553,29 @@ __device__ void schedule_units(const int32_t* __restrict__ ucount, int U, int P,
   if (tid == 0) sk_start[P] = T;
 }
 
+// The schedule (above) as a launch of its own: one workgroup writes tstart, dp_start, sk_start.
+__global__ __launch_bounds__(kPlanThreads) void plan_sched_kernel(const int32_t* __restrict__ ucount, int U, int P,
+                                                                  int32_t* __restrict__ tstart,
+                                                                  int32_t* __restrict__ dp_start,
+                                                                  int32_t* __restrict__ sk_start) {
+  __shared__ int sh[kPlanThreads / 64];
+  __shared__ int unused;
+  schedule_units(ucount, U, P, -1, true, tstart, dp_start, sk_start, sh, &unused);
+}
+
+// Units up to which every workgroup of plan_tiles_kernel computes the schedule itself (each reads
+// all U unit counts, U^2 reads in all) instead of a launch of plan_sched_kernel before it.
+constexpr int kFoldSchedUnits = 1024;
+
 // Expands unit u's union list into one record per 64-key tile at its place in the tile
-// sequence.  Every workgroup computes the schedule (above) for its own unit; workgroup 0 also
-// writes tstart, dp_start and sk_start for the run and the merge.  With kvalid (valid keys at the
-// front of each key block), a tile's padding keys are counted into its flags.
+// sequence.  With fold, every workgroup computes the schedule (above) for its own unit and
+// workgroup 0 also writes tstart, dp_start and sk_start for the run and the merge; otherwise the
+// place is read from tstart, written by plan_sched_kernel.  With kvalid (valid keys at the front
+// of each key block), a tile's padding keys are counted into its flags.
 __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t* __restrict__ ulist,
                                                                   const int32_t* __restrict__ ucount,
                                                                   const int32_t* __restrict__ kvalid, int U,
-                                                                  int P, int32_t* __restrict__ tstart,
+                                                                  int P, bool fold, int32_t* __restrict__ tstart,
                                                                   int32_t* __restrict__ dp_start,
                                                                   int32_t* __restrict__ sk_start, int NK,
                                                                   int block, int row_tiles, int4* __restrict__ trec) {
@@ -568,8 +583,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tiles_kernel(const int32_t*
   __shared__ int first_tile;
   const int u = blockIdx.x;
   const int tid = threadIdx.x;
-  if (tid == 0) first_tile = 0;
-  schedule_units(ucount, U, P, u, u == 0, tstart, dp_start, sk_start, sh, &first_tile);
+  if (fold) {
+    if (tid == 0) first_tile = 0;
+    schedule_units(ucount, U, P, u, u == 0, tstart, dp_start, sk_start, sh, &first_tile);
+  } else if (tid == 0) {
+    first_tile = tstart[u];
+  }
   __syncthreads();
   const int nt = ucount[u], n = nt > 0 ? nt : 1;
   const int nsub = block / KT;
@@ -1111,8 +1130,13 @@ hipError_t launch_attn_plan(const Dims& dm, const int32_t* counts, const int32_t
   hipLaunchKernelGGL(plan_union_kernel, dim3(U), dim3(kPlanThreads), (size_t)((dm.NK + 7) / 8) * sizeof(uint32_t),
                      st, counts, idx, kvalid, dm.NQ, dm.NK, dm.h0, dm.h1, dm.Lk, dm.block, row_tiles, w.qmap,
                      w.ulist, w.ucount);
-  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U,
-                     persistent_workgroups(), w.tstart, w.dp_start, w.sk_start, dm.NK, dm.block, row_tiles, w.trec);
+  const int P = persistent_workgroups();
+  const bool fold = U <= kFoldSchedUnits;
+  if (!fold)
+    hipLaunchKernelGGL(plan_sched_kernel, dim3(1), dim3(kPlanThreads), 0, st, w.ucount, U, P, w.tstart, w.dp_start,
+                       w.sk_start);
+  hipLaunchKernelGGL(plan_tiles_kernel, dim3(U), dim3(kPlanThreads), 0, st, w.ulist, w.ucount, kvalid, U, P, fold,
+                     w.tstart, w.dp_start, w.sk_start, dm.NK, dm.block, row_tiles, w.trec);
   return hipGetLastError();
 }
 
